@@ -1,0 +1,229 @@
+"""Benchmark of the NVFP4 W4A4 linear layer on one MI355X.
+
+Workload (the M = 8192 configuration the headline metric is quoted on): the
+fused MLP gate/up projection, X 8192 x 5120 bf16 with residual-stream
+statistics (seeded synthetic data), W = two separately calibrated segments of
+17408 x 5120 (std 0.015 and 0.0195), Y 8192 x 34816 bf16.
+
+A step is one pass of the hot path: dynamic activation quantization of X
+(amax pass + quantize pass) followed by the NVFP4 GEMM with the per-segment
+scaled epilogue.  The weight prepack is offline and runs once before timing
+(its time is reported separately).  Inputs are resident in HBM before the
+timed region; the 570 MB output written by every step evicts the 256 MB
+MALL, so each step reads X and W from HBM.
+
+value = 2 M N K / (time per step), in TFLOPS.  roofline: the GEMM kernel's
+algorithmic FLOPs per launch over its average launch time measured with HIP
+events on the launch stream, against the FP16 dense MFMA peak (the GEMM
+decodes NVFP4 exactly into FP16 MFMA operands).  cpu_baseline: the CPU oracle
+timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_F16_PEAK_TFLOPS = 2500.0      # MI355X dense FP16/BF16 MFMA
+MXFP4_PEAK_TFLOPS = 10100.0        # MI355X dense FP4 MFMA (reported for context)
+HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
+WORKLOAD = "mlp_gate_up"
+GEMM_SOURCES = ["paper_2609_04098_amd/csrc/gemm.hip", "paper_2609_04098_amd/csrc/packed_layout.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_mlp_gate_up_traffic.md")
+
+
+def log(msg):
+    sys.stderr.write("[bench %s] %s\n" % (time.strftime("%H:%M:%S"), msg))
+    sys.stderr.flush()
+
+
+def gemm_source_hash():
+    h = hashlib.sha256()
+    for p in GEMM_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter summary,
+    if it was taken on the current GEMM source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    m_hash = re.search(r"gemm_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != gemm_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(cfg, x_bits, w_bits, rows=512, cols_per_seg=4096):
+    """The CPU oracle (FP64 numpy, untuned) on a bounded sample of the same
+    workload: quantize `rows` rows of X, then the dequantized GEMM of those
+    rows against `cols_per_seg` rows of each weight segment (quantized
+    beforehand, untimed, like the GPU prepack)."""
+    import numpy as np
+    from oracle import gemm as OG
+    from oracle import quant as OQ
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count()
+    offs = cfg.seg_offsets
+    w_rows = np.concatenate([np.arange(offs[s], offs[s] + cols_per_seg) for s in range(len(offs) - 1)])
+    sub_offs = [cols_per_seg * s for s in range(len(offs))]
+    wp, ws, gw = OQ.quantize_segments(w_bits[w_rows], sub_offs)
+    t0 = time.perf_counter()
+    xp, xs, gx = OQ.quantize_tensor(x_bits[:rows])
+    y = OG.gemm_f64(xp, xs, gx, wp, ws, gw, sub_offs)
+    dt = time.perf_counter() - t0
+    flops = 2.0 * rows * len(w_rows) * cfg.k
+    assert y.shape == (rows, len(w_rows))
+    return {
+        "value": round(flops / dt / 1e12, 6), "unit": "TFLOPS", "cores": int(threads), "kind": "oracle",
+        "sample": "act-quant of %d x %d rows of X + FP64 dequantized GEMM against %d of %d weight rows "
+                  "(%d per segment); %.1f s" % (rows, cfg.k, len(w_rows), cfg.n, cols_per_seg, dt),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build runs the NVFP4 linear layer on a single "
+              "MI355X (no multi-GPU path); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_04098_amd import linear as L
+    from paper_2609_04098_amd import nvfp4 as C
+    from paper_2609_04098_amd import synth
+
+    C.lib()                                      # fail loudly if not built
+    cfg = synth.CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("drawing inputs for %s" % cfg.description)
+    x_bits = synth.make_x(cfg)
+    w_bits = synth.make_w(cfg)
+    to_dev = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(dev)
+    x = to_dev(x_bits)
+    w = to_dev(w_bits)
+    stream = torch.cuda.current_stream()
+
+    # Offline weight prepack (timed separately, not part of a step).
+    t_pack0, t_pack1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_pack0.record(stream)
+    pw = L.pack_weight(w, cfg.seg_offsets)
+    t_pack1.record(stream)
+    torch.cuda.synchronize()
+    prepack_ms = t_pack0.elapsed_time(t_pack1)
+    del w
+
+    aq = L.alloc_act(cfg.m, cfg.k, dev)
+    ws = L.act_workspace(cfg.m, cfg.k, dev)
+    y = torch.empty((cfg.m, cfg.n), dtype=torch.bfloat16, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        L.quantize_act(x, out=aq, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        L.gemm(aq, pw, out=y)
+        if ev is not None:
+            ev[2].record(stream)
+
+    log("warmup %d steps" % args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    log("timing %d steps" % args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    aq_ms = [e[0].elapsed_time(e[1]) for e in events]
+    gemm_ms = [e[1].elapsed_time(e[2]) for e in events]
+    step_ms = [e[0].elapsed_time(e[2]) for e in events]
+    ms_per_step = wall * 1e3 / args.steps
+    flops = cfg.flops
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    gemm_avg = float(np.mean(gemm_ms))
+    aq_avg = float(np.mean(aq_ms))
+    gemm_tflops = flops / (gemm_avg * 1e-3) / 1e12
+    aq_bytes = cfg.m * cfg.k * (2 + 0.5 + 1.0 / 16)
+    aq_gbs = aq_bytes / (aq_avg * 1e-3) / 1e9
+    traffic = committed_traffic()
+    log("step %.3f ms (events %.3f), act-quant %.3f ms, GEMM %.3f ms" % (
+        ms_per_step, float(np.mean(step_ms)), aq_avg, gemm_avg))
+
+    result = {
+        "metric": "NVFP4 W4A4 GEMM TFLOPS incl. act-quant (M=8192) and % of MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "nvfp4",
+        "compute": "E2M1 x E4M3 decoded exactly to f16, v_mfma_f32_32x32x16_f16, f32 accumulate",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: %s" % (cfg.name, cfg.description),
+            "M": cfg.m, "N": cfg.n, "K": cfg.k, "segments": list(cfg.segments),
+            "x": "bf16 N(0,1) with 0.5% channels x U(50,200)", "y": "bf16",
+        },
+        "pct_of_mfma_peak": round(100.0 * value / MFMA_F16_PEAK_TFLOPS, 2),
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "gemm_kernel (NVFP4 GEMM + segment epilogue)",
+            "achieved": round(gemm_tflops, 2),
+            "peak": MFMA_F16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(gemm_tflops / MFMA_F16_PEAK_TFLOPS, 4),
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": flops,
+            "avg_launch_ms": round(gemm_avg, 4),
+        },
+        "act_quant": {
+            "bound": "hbm", "avg_ms": round(aq_avg, 4), "achieved": round(aq_gbs, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(aq_gbs / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes": aq_bytes,
+        },
+        "frac_of_mxfp4_peak": round(value / MXFP4_PEAK_TFLOPS, 4),
+        "prepack_ms": round(prepack_ms, 3),
+        "gemm_source_sha256_16": gemm_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        log("CPU oracle baseline on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(cfg, x_bits, w_bits)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

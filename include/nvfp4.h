@@ -1,0 +1,174 @@
+/*
+ * nvfp4.h -- C ABI of the MI355X (gfx950) NVFP4 W4A4 linear layer.
+ *
+ * NVFP4 (paper, section 2 "NVFP4"): E2M1 4-bit values, one E4M3 scale per
+ * 16-element block set to the block maximum / 6, and one FP32 scale per
+ * tensor.  W4A4: weights and activations are both quantized this way and the
+ * GEMM consumes the 4-bit operands.  Fused modules (paper, section 6,
+ * "Per-module calibration vs. fused-GEMM scaling"): one GEMM serves several
+ * separately calibrated linear modules, so the output columns of each module
+ * (a "segment") carry that module's own FP32 weight scale, and the GEMM
+ * epilogue applies it per segment.
+ *
+ * Numerics (identical in every entry point):
+ *   G      = fl32(2688 / amax) per tensor (2688 = 6 * 448), 0 if amax = 0,
+ *            the largest finite float if the quotient overflows;
+ *   S_b    = RNE_E4M3(amax_b * G / 6) per 16-element block along K,
+ *            saturating at 448, E4M3 subnormals kept (OCP E4M3FN codes);
+ *   code   = sign(x) << 3 | RNE_E2M1(|x| * G / S_b), saturating at 6,
+ *            magnitude 0 when S_b = 0; the sign bit of x is always copied.
+ *   Each rounding is one round-to-nearest-even of the exact real value.
+ *   Codes: byte j of a row holds element 2j in the low nibble and 2j+1 in
+ *   the high nibble.
+ *   GEMM:  Y[m, n] = sum_k (e S)_A[m, k] (e S)_W[n, k] / (G_A * G_W[s(n)]),
+ *          FP32 accumulation; output 0 where G_A * G_W[s] = 0.
+ *
+ * Conventions.
+ *   - All tensor pointers are device pointers, allocated and freed by the
+ *     caller, 16-byte aligned (except the GEMM output, see nvfp4_gemm).
+ *     The library never allocates device memory, keeps no state between
+ *     calls except a per-device property cache, and is safe to call from
+ *     several host threads.
+ *   - Every call validates its arguments synchronously and returns a status
+ *     before anything is enqueued.  Work is enqueued asynchronously on
+ *     ``stream`` (a hipStream_t; NULL is the default stream); no call
+ *     synchronizes the host.
+ *   - Preconditions that are not checked: inputs are finite; buffers do not
+ *     overlap; buffers are at least as large as the stated sizes.
+ *   - Sizes are element counts unless a name ends in _bytes.
+ */
+#ifndef NVFP4_H
+#define NVFP4_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+enum nvfp4_status {
+  NVFP4_OK = 0,
+  NVFP4_EINVAL = 1,        /* null or misaligned pointer, bad shape/stride/mode/segment table */
+  NVFP4_EUNSUPPORTED = 2,  /* the current HIP device is not gfx950 */
+  NVFP4_EWORKSPACE = 3,    /* workspace or packed buffer smaller than required */
+  NVFP4_EHIP = 4           /* a HIP runtime call or kernel launch failed */
+};
+
+/* Global-scale mode of a quantization call. */
+enum nvfp4_scale_mode {
+  NVFP4_DYNAMIC = 0,       /* G computed from the tensor amax on the device and written out */
+  NVFP4_STATIC = 1         /* G read from the device scalar(s) passed in (a calibrated scale) */
+};
+
+/* Output element type of nvfp4_gemm. */
+enum nvfp4_out_dtype {
+  NVFP4_OUT_BF16 = 0,      /* round-to-nearest-even of the FP32 result */
+  NVFP4_OUT_F32 = 1
+};
+
+#define NVFP4_BLOCK 16          /* elements per block scale, along K */
+#define NVFP4_MAX_SEGMENTS 8    /* fused segments per GEMM */
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* nvfp4_status_string(int status);
+
+/* The hipError_t value of the last NVFP4_EHIP failure on the calling host
+ * thread (0 if none). */
+int nvfp4_last_hip_error(void);
+
+/* Workspace bytes nvfp4_quantize_act needs for an M x K activation (the
+ * per-workgroup partial maxima of the dynamic global scale); 0 is a valid
+ * answer only in static mode, and the dynamic answer is returned here. */
+size_t nvfp4_quantize_act_workspace_bytes(int64_t M, int64_t K);
+
+/*
+ * Dynamic activation quantization (paper, section 2: NVFP4; section 9
+ * "Decode overhead": the activation side is quantized at run time).
+ *
+ *   x        bf16 [M x K], row stride ldx elements (ldx >= K, ldx % 8 == 0).
+ *   codes    out, uint8 [M x K/2] row-major (packed E2M1 pairs, see above).
+ *   scales   out, uint8 [M x K/16] row-major E4M3 codes, one per block.
+ *   g_enc    one device float: written with G in NVFP4_DYNAMIC mode, read in
+ *            NVFP4_STATIC mode (must then be finite and >= 0).
+ *   workspace, workspace_bytes: device scratch of at least
+ *            nvfp4_quantize_act_workspace_bytes(M, K) bytes in dynamic mode;
+ *            unused in static mode (may be NULL).  Its contents on entry do
+ *            not matter; calls sharing one workspace must be ordered.
+ * Requirements: M >= 0, K >= 0, K % 16 == 0, M * K < 2^31.
+ * Errors: NVFP4_EINVAL, NVFP4_EWORKSPACE, NVFP4_EUNSUPPORTED, NVFP4_EHIP.
+ * M == 0 or K == 0 writes G = 0 in dynamic mode and nothing else.
+ */
+int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
+                       uint8_t* codes, uint8_t* scales, float* g_enc, int mode,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
+ * tile layout of the codes and block scales, N padded to 32 and K to 256. */
+size_t nvfp4_packed_weight_bytes(int64_t N, int64_t K);
+
+/* Workspace bytes nvfp4_pack_weight needs (per-segment partial maxima). */
+size_t nvfp4_pack_weight_workspace_bytes(int64_t N, int64_t K, int n_seg);
+
+/*
+ * Weight quantization and prepack (offline).  The rows of W are the output
+ * columns of the GEMM; rows [seg_offsets[s], seg_offsets[s+1]) form segment
+ * s, a separately calibrated module with its own global scale (paper,
+ * section 6: one FP32 global scale per linear module).
+ *
+ *   w            bf16 [N x K], row stride ldw elements (ldw >= K, ldw % 8 == 0).
+ *   seg_offsets  HOST array of n_seg + 1 entries, strictly increasing from 0
+ *                to N; 1 <= n_seg <= NVFP4_MAX_SEGMENTS.
+ *   g_enc_seg    device float [n_seg]: written with each segment's G in
+ *                NVFP4_DYNAMIC mode (from that segment's amax), read in
+ *                NVFP4_STATIC mode.
+ *   packed       out, device buffer of packed_bytes >=
+ *                nvfp4_packed_weight_bytes(N, K) bytes; its layout is private
+ *                to nvfp4_gemm (nvfp4_unpack_weight gives the canonical form).
+ *   workspace    device scratch of nvfp4_pack_weight_workspace_bytes bytes
+ *                (dynamic mode; may be NULL in static mode).
+ * Requirements: N >= 1, K >= 16, K % 16 == 0, N * K < 2^31.
+ */
+int nvfp4_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
+                      const int64_t* seg_offsets, int n_seg, float* g_enc_seg,
+                      int mode, void* packed, size_t packed_bytes,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Inverse of the prepack layout, for verification: writes the canonical
+ * codes uint8 [N x K/2] and scales uint8 [N x K/16] of a packed weight.
+ */
+int nvfp4_unpack_weight(const void* packed, int64_t N, int64_t K,
+                        uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
+ * NVFP4 x NVFP4 GEMM with FP32 accumulation and a per-segment scaled
+ * epilogue (paper, section 2: W4A4 GEMM on 4-bit operands; section 6: each
+ * fused segment scaled by its own module's global scale).
+ *
+ *   a_codes, a_scales  the activation as written by nvfp4_quantize_act
+ *                      ([M x K/2] and [M x K/16], contiguous rows).
+ *   a_g_enc            device float: G_A.
+ *   w_packed           the weight as written by nvfp4_pack_weight for the
+ *                      same N and K.
+ *   seg_offsets        HOST array, as for nvfp4_pack_weight (same segments).
+ *   w_g_enc_seg        device float [n_seg]: G_W per segment.
+ *   y                  out, [M x N] with row stride ldy elements (ldy >= N),
+ *                      bf16 or float per y_dtype, aligned to its element size.
+ *   Y[m, n] = (1 / (G_A * G_W[s])) * sum_k (e S)_A[m, k] (e S)_W[n, k]
+ *   for the segment s holding column n.
+ * Requirements: M >= 0, N >= 1, K >= 16, K % 16 == 0, M*K, N*K, M*ldy < 2^31.
+ * M == 0 enqueues nothing.
+ */
+int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
+               const float* a_g_enc, int64_t M, int64_t K,
+               const void* w_packed, int64_t N,
+               const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg,
+               void* y, int64_t ldy, int y_dtype, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NVFP4_H */

@@ -1,0 +1,168 @@
+// Dynamic activation quantization to NVFP4 on gfx950 (paper, section 2
+// "NVFP4"; the run-time "A4" half of W4A4).
+//
+// Two launches on the caller's stream, no atomics and no memset:
+//   1. amax_partial: each workgroup reduces |x| over a grid-strided share of
+//      X and writes one partial maximum to the workspace.  bf16 magnitudes
+//      order like unsigned integers, so the reduction is packed u16 max.
+//   2. quantize: every workgroup first reduces the partials to amax_X and
+//      forms G = fl32(2688 / amax_X) (workgroup 0 writes it out), then each
+//      thread quantizes 16-element blocks: 32 bytes of bf16 in, 8 bytes of
+//      packed E2M1 codes and 1 byte of E4M3 scale out.
+// In static mode pass 1 is skipped and G is read from the caller's scalar.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "launch.h"
+#include "quant_device.h"
+
+namespace nvfp4 {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    uint32_t o = __shfl_xor(v, off, 64);
+    v = v > o ? v : o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* lds) {
+  v = wave_max_u32(v);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) lds[wave] = v;
+  __syncthreads();
+  uint32_t r = lds[0];
+#pragma unroll
+  for (int w = 1; w < kThreads / 64; ++w) r = r > lds[w] ? r : lds[w];
+  __syncthreads();
+  return r;
+}
+
+// Address of 16-byte vector `v` (8 bf16) of X: contiguous rows or stride ldx.
+template <bool kContig>
+__device__ __forceinline__ const uint4* vec_ptr(const uint16_t* x, uint32_t v, uint32_t vec_per_row,
+                                                uint32_t ldx) {
+  if (kContig) return reinterpret_cast<const uint4*>(x) + v;
+  uint32_t row = v / vec_per_row, col = v - row * vec_per_row;
+  return reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + col;
+}
+
+template <bool kContig>
+__global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* __restrict__ x,
+                                                                uint32_t n_vec, uint32_t vec_per_row,
+                                                                uint32_t ldx, float* __restrict__ partial) {
+  __shared__ uint32_t lds[kThreads / 64];
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 m = {0, 0};
+  const uint32_t stride = gridDim.x * kThreads;
+  uint32_t v = blockIdx.x * kThreads + threadIdx.x;
+  // Four independent 16-byte loads in flight per thread.
+  for (; v + 3 * stride < n_vec; v += 4 * stride) {
+    uint4 d[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) d[u] = *vec_ptr<kContig>(x, v + u * stride, vec_per_row, ldx);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d[u].x & 0x7FFF7FFFu));
+      m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d[u].y & 0x7FFF7FFFu));
+      m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d[u].z & 0x7FFF7FFFu));
+      m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d[u].w & 0x7FFF7FFFu));
+    }
+  }
+  for (; v < n_vec; v += stride) {
+    uint4 d = *vec_ptr<kContig>(x, v, vec_per_row, ldx);
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d.x & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d.y & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d.z & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d.w & 0x7FFF7FFFu));
+  }
+  uint32_t mx = m[0] > m[1] ? m[0] : m[1];
+  mx = block_max_u32(mx, lds);
+  if (threadIdx.x == 0) partial[blockIdx.x] = __uint_as_float(mx << 16);
+}
+
+template <bool kDynamic, bool kContig>
+__global__ __launch_bounds__(kThreads) void act_quant_kernel(
+    const uint16_t* __restrict__ x, uint32_t n_blocks, uint32_t blocks_per_row, uint32_t ldx,
+    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ g_enc,
+    const float* __restrict__ partial, uint32_t n_partial) {
+  __shared__ uint32_t lds[kThreads / 64];
+  float g;
+  if (kDynamic) {
+    uint32_t m = 0;
+    for (uint32_t i = threadIdx.x; i < n_partial; i += kThreads) {
+      uint32_t p = __float_as_uint(partial[i]);
+      m = m > p ? m : p;                       // non-negative floats order as integers
+    }
+    g = global_scale(__uint_as_float(block_max_u32(m, lds)));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *g_enc = g;
+  } else {
+    g = *g_enc;
+  }
+  const float gd6 = g * (1.0f / 6.0f);
+  const uint32_t stride = gridDim.x * kThreads;
+  for (uint32_t b = blockIdx.x * kThreads + threadIdx.x; b < n_blocks; b += stride) {
+    const uint4* src;
+    if (kContig) {
+      src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
+    } else {
+      uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
+      src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+    }
+    uint4 d0 = src[0], d1 = src[1];
+    uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    uint32_t c0, c1;
+    uint32_t sc = quantize_block(v, g, gd6, c0, c1);
+    reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
+    scales[b] = (uint8_t)sc;
+  }
+}
+
+__global__ void write_zero_scale_kernel(float* g_enc) { *g_enc = 0.0f; }
+
+static int grid_for(uint64_t work_items, int cap) {
+  uint64_t g = (work_items + kThreads - 1) / kThreads;
+  if (g > (uint64_t)cap) g = cap;
+  return g < 1 ? 1 : (int)g;
+}
+
+hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
+                            uint8_t* scales, float* g_enc, bool dynamic, float* partial,
+                            hipStream_t stream) {
+  if (M == 0 || K == 0) {
+    if (dynamic) hipLaunchKernelGGL(write_zero_scale_kernel, dim3(1), dim3(1), 0, stream, g_enc);
+    return hipGetLastError();
+  }
+  const bool contig = (ldx == K);
+  const uint16_t* xp = static_cast<const uint16_t*>(x);
+  const uint32_t n_vec = (uint32_t)(M * K / 8), vec_per_row = (uint32_t)(K / 8);
+  const uint32_t n_blocks = (uint32_t)(M * K / 16), blocks_per_row = (uint32_t)(K / 16);
+  int n_partial = 0;
+  if (dynamic) {
+    n_partial = grid_for(n_vec / 4, kActPartials);
+    if (contig)
+      hipLaunchKernelGGL(amax_partial_kernel<true>, dim3(n_partial), dim3(kThreads), 0, stream, xp,
+                         n_vec, vec_per_row, (uint32_t)ldx, partial);
+    else
+      hipLaunchKernelGGL(amax_partial_kernel<false>, dim3(n_partial), dim3(kThreads), 0, stream, xp,
+                         n_vec, vec_per_row, (uint32_t)ldx, partial);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int grid = grid_for(n_blocks, kActQuantGridCap);
+#define NVFP4_AQ(D, C)                                                                          \
+  hipLaunchKernelGGL((act_quant_kernel<D, C>), dim3(grid), dim3(kThreads), 0, stream, xp, n_blocks, \
+                     blocks_per_row, (uint32_t)ldx, codes, scales, g_enc, partial, (uint32_t)n_partial)
+  if (dynamic) {
+    if (contig) NVFP4_AQ(true, true); else NVFP4_AQ(true, false);
+  } else {
+    if (contig) NVFP4_AQ(false, true); else NVFP4_AQ(false, false);
+  }
+#undef NVFP4_AQ
+  return hipGetLastError();
+}
+
+}  // namespace nvfp4

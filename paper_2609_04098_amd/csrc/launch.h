@@ -1,0 +1,36 @@
+// Host-side launchers of the NVFP4 kernels (called by api.cpp after argument
+// validation) and the constants that size their workspaces.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Entries of the segment-offset table passed to kernels (max segments + 1).
+#define NVFP4_SEG_TABLE 9
+
+namespace nvfp4 {
+
+// Partial maxima written by the activation amax pass (one per workgroup).
+constexpr int kActPartials = 1024;
+// Upper bound on quantize workgroups (grid-strided beyond that).
+constexpr int kActQuantGridCap = 4096;
+// Partial maxima per weight segment.
+constexpr int kWeightPartials = 256;
+
+hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
+                            uint8_t* scales, float* g_enc, bool dynamic, float* partial,
+                            hipStream_t stream);
+
+hipError_t launch_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
+                              const int64_t* seg_offsets, int n_seg, float* g_enc_seg,
+                              bool dynamic, void* packed, float* partial, hipStream_t stream);
+
+hipError_t launch_unpack_weight(const void* packed, int64_t N, int64_t K, uint8_t* codes,
+                                uint8_t* scales, hipStream_t stream);
+
+hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                       int64_t M, int64_t K, const void* w_packed, int64_t N,
+                       const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
+                       int64_t ldy, bool out_f32, hipStream_t stream);
+
+}  // namespace nvfp4

@@ -1,0 +1,142 @@
+// Device-side NVFP4 block quantization for gfx950 (used by the activation
+// quantizer and the weight prepack; never by host code).
+//
+// Definition (paper, section 2 "NVFP4"): one E4M3 scale per 16-element block
+// set to block max / 6 under the per-tensor FP32 global scale G, elements in
+// E2M1.  Every rounding is one round-to-nearest-even of the exact real value:
+//
+//   S    = RNE_E4M3(amax_b * G / 6)       (OCP E4M3FN, saturating at 448)
+//   code = sign(x) | RNE_E2M1(|x| G / S)   (saturating at 6; 0 when S = 0)
+//
+// How the exact decision is reached in binary32 (no wide arithmetic):
+// a value u is compared with the rounding midpoints of its target format.
+// All midpoints lie on a "lattice" that is cheap to round to (for E2M1,
+// q = 4 v is compared with integers; for E4M3, the grid refined by one bit).
+// We round an approximation of u to the nearest lattice point L (off by far
+// less than half a lattice step), then get the exact sign of u - L from one
+// fused multiply-add: fma(a, G, -c L) rounds the exact value a G - c L once,
+// which keeps its sign and its zero-ness (a G has <= 32 significant bits, c L
+// <= 11, so the only rounding is of a non-zero difference).  Moving L by one
+// ulp in that direction gives a binary32 value w that lies strictly on the
+// same side as u of every midpoint, and equals a midpoint exactly when u
+// does; a hardware round-to-nearest-even of w then gives the exact result.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nvfp4 {
+
+constexpr float kRange = 2688.0f;             // 6 (E2M1 max) * 448 (E4M3 max)
+constexpr float kFltMax = 3.40282347e+38f;
+
+__device__ __forceinline__ float bf16_lo(uint32_t d) { return __uint_as_float(d << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t d) { return __uint_as_float(d & 0xFFFF0000u); }
+
+__device__ __forceinline__ int sign3(float e) {
+  // -1, 0, +1 for e < 0, e == +0, e > 0 (e is never -0.0 here: an exact
+  // zero from fma is +0 under round-to-nearest-even).  NaN maps to +-1.
+  int b = (int)__float_as_uint(e);
+  return b < -1 ? -1 : (b > 1 ? 1 : b);
+}
+
+// Per-tensor global scale G = fl32(2688 / amax); 0 for amax = 0; overflow
+// saturates to the largest finite binary32 value.  The division is the
+// correctly rounded IEEE division (built with correctly rounded fp32 divide).
+__device__ __forceinline__ float global_scale(float amax) {
+  if (amax == 0.0f) return 0.0f;
+  return fminf(kRange / amax, kFltMax);
+}
+
+// Max of the bf16 magnitudes of 8 packed dwords (16 elements), as a float.
+__device__ __forceinline__ float block_amax(const uint32_t v[8]) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 m = __builtin_bit_cast(u16x2, v[0] & 0x7FFF7FFFu);
+#pragma unroll
+  for (int i = 1; i < 8; ++i)
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, v[i] & 0x7FFF7FFFu));
+  uint32_t mx = m[0] > m[1] ? m[0] : m[1];
+  return __uint_as_float(mx << 16);
+}
+
+// E4M3 code of RNE_E4M3(amax_b * G / 6), exactly.  gd6 is any approximation
+// of G / 6 within a few ulps.
+__device__ __forceinline__ uint32_t scale_code(float amax_b, float g, float gd6) {
+  float ua = amax_b * gd6;                           // ~ amax_b G / 6
+  // Nearest point of the lattice {E4M3 values and midpoints}: multiples of
+  // 2^(e-4) in binade [2^e, 2^(e+1)) for e >= -6, multiples of 2^-10 below.
+  float l_norm = __uint_as_float((__float_as_uint(ua) + 0x40000u) & 0xFFF80000u);
+  float l_sub = __builtin_rintf(ua * 1024.0f) * 0x1p-10f;
+  float l = ua >= 0x1p-6f ? l_norm : l_sub;
+  int s = sign3(__builtin_fmaf(amax_b, g, -6.0f * l)); // sign(amax_b G - 6 L)
+  float w = __uint_as_float(__float_as_uint(l) + (uint32_t)s);
+  // RNE of w onto E4M3 (w >= 0): subnormal range by rint, else round the
+  // binary32 significand to 3 bits; saturate to 448 (code 126).
+  uint32_t code_sub = (uint32_t)__builtin_rintf(w * 512.0f);
+  uint32_t b = __float_as_uint(w);
+  uint32_t code_norm = ((b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20) - 960u;
+  code_norm = code_norm < 126u ? code_norm : 126u;
+  return w < 0x1p-6f ? code_sub : code_norm;
+}
+
+// Value of an E4M3 scale code (OCP E4M3FN; the hardware conversion).
+__device__ __forceinline__ float scale_value(uint32_t code) {
+  return __builtin_amdgcn_cvt_f32_fp8((int)code, 0);
+}
+
+struct ElemConsts {
+  float g;      // G
+  float grq;    // ~ G / (S / 4)   (0 when S = 0)
+  float sq;     // S / 4, exact
+};
+
+__device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
+  ElemConsts c;
+  c.g = g;
+  c.sq = s * 0.25f;
+  // Clamped so that a saturated G (tensor amax below 2688 / FLT_MAX) cannot
+  // turn 0 * grq into NaN; any finite grq at least as large gives q >= 64
+  // for every non-zero |x|, which is the saturated code either way.
+  c.grq = s > 0.0f ? __builtin_fminf(g * (4.0f * __builtin_amdgcn_rcpf(s)), kFltMax) : 0.0f;
+  return c;
+}
+
+// Binary32 value w with the sign of x such that RNE_E2M1(w / 4) equals
+// RNE_E2M1(|x| G / S) exactly (see the header comment): q = 4 |x| G / S is
+// compared with the integers 1, 3, 5, 7, 10, 14, 20 (four times the E2M1
+// midpoints).  q is clamped at 64, beyond every midpoint, so that a static
+// scale that overflows the range still saturates.
+__device__ __forceinline__ float e2m1_arg(float x, const ElemConsts& c) {
+  float ax = __builtin_fabsf(x);
+  float q = __builtin_fminf(ax * c.grq, 64.0f);
+  float n = __builtin_rintf(q);
+  int s = sign3(__builtin_fmaf(ax, c.g, -(n * c.sq)));   // sign(|x| G - n S/4)
+  uint32_t w = __float_as_uint(n) + (uint32_t)s;
+  return __uint_as_float(w | (__float_as_uint(x) & 0x80000000u));
+}
+
+// Packed codes of 8 elements (4 dwords of bf16 pairs); element 2j goes to
+// the low nibble of byte j.  The conversion divides by 2^exponent(4.0) = 4
+// and rounds to nearest even with saturation.
+__device__ __forceinline__ uint32_t encode8(const uint32_t* d, const ElemConsts& k) {
+  uint32_t r = 0u;
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[0]), k), e2m1_arg(bf16_hi(d[0]), k), 4.0f, 0);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[1]), k), e2m1_arg(bf16_hi(d[1]), k), 4.0f, 1);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[2]), k), e2m1_arg(bf16_hi(d[2]), k), 4.0f, 2);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[3]), k), e2m1_arg(bf16_hi(d[3]), k), 4.0f, 3);
+  return r;
+}
+
+// Quantize one block: 8 dwords of bf16 pairs -> 2 dwords of packed codes;
+// returns the E4M3 scale code.
+__device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g, float gd6,
+                                                   uint32_t& c0, uint32_t& c1) {
+  float amax_b = block_amax(v);
+  uint32_t sc = scale_code(amax_b, g, gd6);
+  ElemConsts k = elem_consts(g, scale_value(sc));
+  c0 = encode8(v, k);
+  c1 = encode8(v + 4, k);
+  return sc;
+}
+
+}  // namespace nvfp4

@@ -1,0 +1,102 @@
+"""NVFP4 W4A4 linear layer on top of the C ABI: buffer allocation and call
+order only (the arithmetic is in the HIP kernels).
+
+    pw = pack_weight(w, seg_offsets)          # offline: quantize + prepack W
+    aq = quantize_act(x)                      # per call: codes, scales, G_A
+    y  = gemm(aq, pw)                         # Y = dq(A) dq(W)^T, segment-scaled
+"""
+
+from dataclasses import dataclass
+from typing import List
+
+import torch
+
+from . import nvfp4 as _c
+
+
+@dataclass
+class PackedWeight:
+    packed: torch.Tensor          # uint8, GEMM-private layout
+    g_seg: torch.Tensor           # float32 [n_seg], encode-direction global scales
+    n: int
+    k: int
+    seg_offsets: List[int]
+
+
+@dataclass
+class QuantizedAct:
+    codes: torch.Tensor           # uint8 [M, K/2]
+    scales: torch.Tensor          # uint8 [M, K/16] (E4M3 codes)
+    g: torch.Tensor               # float32 [1]
+    m: int
+    k: int
+
+
+def _dev(t):
+    return t.device
+
+
+def pack_weight(w, seg_offsets=None, g_seg=None, stream=None) -> PackedWeight:
+    """Quantize a bf16 [N, K] weight whose row ranges are separately
+    calibrated segments; dynamic per-segment scales unless g_seg is given."""
+    n, k = w.shape
+    seg_offsets = [0, n] if seg_offsets is None else [int(o) for o in seg_offsets]
+    n_seg = len(seg_offsets) - 1
+    dev = _dev(w)
+    packed = torch.empty(_c.nvfp4_packed_weight_bytes(n, k), dtype=torch.uint8, device=dev)
+    if g_seg is None:
+        gs = torch.empty(n_seg, dtype=torch.float32, device=dev)
+        ws = torch.empty(_c.nvfp4_pack_weight_workspace_bytes(n, k, n_seg), dtype=torch.uint8, device=dev)
+        _c.nvfp4_pack_weight(w, seg_offsets, gs, packed, _c.NVFP4_DYNAMIC, ws, stream)
+    else:
+        gs = torch.as_tensor(g_seg, dtype=torch.float32).to(dev).contiguous()
+        _c.nvfp4_pack_weight(w, seg_offsets, gs, packed, _c.NVFP4_STATIC, None, stream)
+    return PackedWeight(packed, gs, n, k, seg_offsets)
+
+
+def unpack_weight(pw: PackedWeight, stream=None):
+    """Canonical (codes uint8 [N, K/2], scales uint8 [N, K/16]) of a packed weight."""
+    dev = pw.packed.device
+    codes = torch.empty((pw.n, pw.k // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((pw.n, pw.k // 16), dtype=torch.uint8, device=dev)
+    _c.nvfp4_unpack_weight(pw.packed, pw.n, pw.k, codes, scales, stream)
+    return codes, scales
+
+
+def alloc_act(m, k, device) -> QuantizedAct:
+    return QuantizedAct(torch.empty((m, k // 2), dtype=torch.uint8, device=device),
+                        torch.empty((m, k // 16), dtype=torch.uint8, device=device),
+                        torch.empty(1, dtype=torch.float32, device=device), m, k)
+
+
+def act_workspace(m, k, device):
+    return torch.empty(_c.nvfp4_quantize_act_workspace_bytes(m, k), dtype=torch.uint8, device=device)
+
+
+def quantize_act(x, g=None, out: QuantizedAct = None, workspace=None, stream=None) -> QuantizedAct:
+    """Quantize a bf16 [M, K] activation (dynamic G unless ``g`` is given)."""
+    m, k = x.shape
+    dev = _dev(x)
+    aq = alloc_act(m, k, dev) if out is None else out
+    if g is None:
+        ws = act_workspace(m, k, dev) if workspace is None else workspace
+        _c.nvfp4_quantize_act(x, aq.codes, aq.scales, aq.g, _c.NVFP4_DYNAMIC, ws, stream)
+    else:
+        aq.g.copy_(torch.as_tensor([float(g)], dtype=torch.float32))
+        _c.nvfp4_quantize_act(x, aq.codes, aq.scales, aq.g, _c.NVFP4_STATIC, None, stream)
+    return aq
+
+
+def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None, stream=None):
+    if aq.k != pw.k:
+        raise ValueError("K mismatch between activation and weight")
+    y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=aq.codes.device)
+    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    _c.nvfp4_gemm(aq.codes, aq.scales, aq.g, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, kind,
+                  stream, M=aq.m, K=aq.k)
+    return y
+
+
+def linear(x, pw: PackedWeight, out_dtype=torch.bfloat16):
+    """y = x W^T through NVFP4 W4A4: dynamic act-quant, then the GEMM."""
+    return gemm(quantize_act(x), pw, out_dtype)

@@ -1,0 +1,124 @@
+"""The C-ABI library loads, exports every function include/nvfp4.h declares,
+and rejects invalid arguments synchronously, before any HIP call (these paths
+need no GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_04098_amd import nvfp4 as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nvfp4.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nvfp4_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ["nvfp4_quantize_act", "nvfp4_pack_weight", "nvfp4_gemm", "nvfp4_unpack_weight"]:
+        assert n in names
+    assert set(names) == set(C.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = C.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = C.lib()
+    for s in range(5):
+        assert lib.nvfp4_status_string(s).decode().startswith("NVFP4")
+    assert lib.nvfp4_last_hip_error() == 0
+
+
+def test_sizes():
+    lib = C.lib()
+    assert lib.nvfp4_quantize_act_workspace_bytes(8192, 5120) >= 4
+    # N padded to 32, K to 256: codes Np*Kp/2 + scales Np*Kp/16
+    assert lib.nvfp4_packed_weight_bytes(96, 5120) == 96 * 5120 // 2 + 96 * 5120 // 16
+    assert lib.nvfp4_packed_weight_bytes(100, 80) == 128 * 256 // 2 + 128 * 256 // 16
+    assert lib.nvfp4_packed_weight_bytes(0, 80) == 0
+    assert lib.nvfp4_pack_weight_workspace_bytes(10, 32, 3) >= 3 * 4
+
+
+FAKE = 0x100000   # 16-byte aligned, never dereferenced: validation fails first
+
+
+def _offs(lst):
+    return (ctypes.c_int64 * len(lst))(*lst)
+
+
+def test_quantize_act_rejects_bad_arguments():
+    f = C.lib().nvfp4_quantize_act
+    ws = C.lib().nvfp4_quantize_act_workspace_bytes(4, 32)
+    ok = dict(x=FAKE, M=4, K=32, ldx=32, codes=FAKE, scales=FAKE, g=FAKE, mode=0, ws=FAKE, wsb=ws)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["x"], a["M"], a["K"], a["ldx"], a["codes"], a["scales"], a["g"], a["mode"],
+                 a["ws"], a["wsb"], None)
+    assert call(K=24) == C.NVFP4_EINVAL             # K % 16 != 0
+    assert call(M=-1) == C.NVFP4_EINVAL
+    assert call(ldx=16) == C.NVFP4_EINVAL           # ldx < K
+    assert call(ldx=36) == C.NVFP4_EINVAL           # ldx % 8 != 0
+    assert call(x=None) == C.NVFP4_EINVAL
+    assert call(codes=FAKE + 4) == C.NVFP4_EINVAL   # misaligned
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert call(mode=7) == C.NVFP4_EINVAL
+    assert call(ws=None) == C.NVFP4_EINVAL
+    assert call(wsb=ws - 1) == C.NVFP4_EWORKSPACE
+    assert call(M=1 << 20, K=1 << 12, ldx=1 << 12) == C.NVFP4_EINVAL   # M*K >= 2^31
+
+
+def test_pack_weight_rejects_bad_arguments():
+    f = C.lib().nvfp4_pack_weight
+    n, k = 64, 256
+    pb = C.lib().nvfp4_packed_weight_bytes(n, k)
+    wsb = C.lib().nvfp4_pack_weight_workspace_bytes(n, k, 2)
+
+    def call(offs=(0, 32, 64), n_seg=2, N=n, K=k, ldw=k, packed_bytes=pb, ws=FAKE, mode=0, g=FAKE):
+        return f(FAKE, N, K, ldw, _offs(list(offs)), n_seg, g, mode, FAKE, packed_bytes, ws, wsb, None)
+    assert call(offs=(0, 32, 32), n_seg=2) == C.NVFP4_EINVAL       # not strictly increasing
+    assert call(offs=(0, 32, 60), n_seg=2) == C.NVFP4_EINVAL       # does not end at N
+    assert call(offs=(1, 32, 64), n_seg=2) == C.NVFP4_EINVAL       # does not start at 0
+    assert call(offs=tuple(range(0, 72, 8)), n_seg=9, N=64) == C.NVFP4_EINVAL  # > 8 segments
+    assert call(n_seg=0) == C.NVFP4_EINVAL
+    assert call(K=8, ldw=8) == C.NVFP4_EINVAL
+    assert call(packed_bytes=pb - 1) == C.NVFP4_EWORKSPACE
+    assert call(ws=None) == C.NVFP4_EINVAL
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert f(FAKE, n, k, k, None, 1, FAKE, 0, FAKE, pb, FAKE, wsb, None) == C.NVFP4_EINVAL
+
+
+def test_gemm_rejects_bad_arguments():
+    f = C.lib().nvfp4_gemm
+
+    def call(M=16, K=64, N=32, offs=(0, 32), n_seg=1, ldy=32, dtype=0, y=FAKE, a=FAKE, wg=FAKE):
+        return f(a, FAKE, FAKE, M, K, FAKE, N, _offs(list(offs)), n_seg, wg, y, ldy, dtype, None)
+    assert call(K=40) == C.NVFP4_EINVAL
+    assert call(K=0) == C.NVFP4_EINVAL
+    assert call(N=0, offs=(0, 0)) == C.NVFP4_EINVAL
+    assert call(ldy=24) == C.NVFP4_EINVAL
+    assert call(y=FAKE + 2, dtype=1) == C.NVFP4_EINVAL     # f32 output not 4-byte aligned
+    assert call(dtype=5) == C.NVFP4_EINVAL
+    assert call(offs=(0, 16, 32), n_seg=1) == C.NVFP4_EINVAL
+    assert call(y=None) == C.NVFP4_EINVAL
+    assert call(a=FAKE + 8) == C.NVFP4_EINVAL
+    assert call(wg=None) == C.NVFP4_EINVAL
+    assert f(FAKE, FAKE, FAKE, 16, 64, FAKE, 32, None, 1, FAKE, FAKE, 32, 0, None) == C.NVFP4_EINVAL
+
+
+def test_unpack_rejects_bad_arguments():
+    f = C.lib().nvfp4_unpack_weight
+    assert f(FAKE, 0, 32, FAKE, FAKE, None) == C.NVFP4_EINVAL
+    assert f(FAKE, 8, 24, FAKE, FAKE, None) == C.NVFP4_EINVAL
+    assert f(None, 8, 32, FAKE, FAKE, None) == C.NVFP4_EINVAL

@@ -1,0 +1,145 @@
+"""GPU parity of the NVFP4 GEMM (nvfp4_gemm) against the CPU oracle.
+
+FP32 output: per element |Y - Y_ref| <= 1e-4 * sum_k |a_k w_k| and relative
+Frobenius error <= 1e-5 (tests/gpu_common.py).  BF16 output: equal to the
+round-to-nearest-even of the same kernel's FP32 output.  Small and ragged
+shapes are checked on every element; the full workloads on sampled rows
+(all columns of each sampled row)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import gemm as OG
+from oracle import quant as OQ
+from paper_2609_04098_amd import linear as L
+from paper_2609_04098_amd import synth
+from tests.gpu_common import bf16_rne_of, check_gemm, log, np_u8, to_dev_bf16, workload
+
+pytestmark = pytest.mark.gpu
+
+
+def bits_of(v):
+    return synth.f64_to_bf16_bits(np.asarray(v, dtype=np.float64))
+
+
+def run_gpu(x_bits, w_bits, offs, ldy=None):
+    """Quantize, pack and multiply on the GPU; returns (y32, y16 bits, aq, pw)."""
+    m, n = x_bits.shape[0], w_bits.shape[0]
+    aq = L.quantize_act(to_dev_bf16(x_bits))
+    pw = L.pack_weight(to_dev_bf16(w_bits), offs)
+    ldy = n if ldy is None else ldy
+    y32 = torch.empty((m, ldy), dtype=torch.float32, device="cuda")[:, :n]
+    y16 = torch.empty((m, ldy), dtype=torch.bfloat16, device="cuda")[:, :n]
+    L.gemm(aq, pw, out=y32)
+    L.gemm(aq, pw, out=y16)
+    torch.cuda.synchronize()
+    return y32, y16, aq, pw
+
+
+def oracle_all(x_bits, w_bits, offs):
+    xp, xs, gx = OQ.quantize_tensor(x_bits)
+    wp, ws, gw = OQ.quantize_segments(w_bits, offs)
+    y = OG.gemm_exact(xp, xs, gx, wp, ws, gw, offs)
+    r = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
+    return y, r
+
+
+def check_small(x_bits, w_bits, offs, ldy=None, what=""):
+    y32, y16, _, _ = run_gpu(x_bits, w_bits, offs, ldy)
+    y_ref, r_ref = oracle_all(x_bits, w_bits, offs)
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, what)
+    np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_of(y32.contiguous()))
+
+
+def _xw(rng, m, n, k, outliers=True):
+    x = rng.standard_normal((m, k))
+    if outliers:
+        x[:, rng.choice(k, max(1, k // 200), replace=False)] *= 100.0
+    w = rng.standard_normal((n, k)) * 0.02
+    return bits_of(x), bits_of(w)
+
+
+def test_gemm_tiny_workload():
+    cfg = synth.CONFIGS["tiny"]
+    check_small(synth.make_x(cfg), synth.make_w(cfg), cfg.seg_offsets, what="tiny")
+
+
+@pytest.mark.parametrize("m,n,k,offs", [
+    (100, 72, 80, [0, 40, 72]),            # K % 64 == 16: unaligned-K path, ragged M/N
+    (300, 300, 320, [0, 1, 299, 300]),     # 2 x 2 tiles, K % 256 != 0, 1-column segments
+    (257, 96, 512, [0, 48, 96]),           # tall-skinny path, 48 + 48 segments in one tile
+    (64, 40, 48, [0, 40]),                 # tall-skinny path, N not a multiple of 32
+    (1, 33, 16, [0, 33]),                  # single row, single block
+    (513, 520, 1024, [0, 100, 200, 300, 400, 500, 510, 515, 520]),   # 8 segments
+])
+def test_gemm_ragged_shapes(m, n, k, offs):
+    rng = np.random.default_rng(m * 7 + n * 3 + k)
+    x, w = _xw(rng, m, n, k)
+    check_small(x, w, offs, what="%dx%dx%d" % (m, n, k))
+
+
+def test_gemm_strided_output():
+    rng = np.random.default_rng(300)
+    x, w = _xw(rng, 70, 136, 256)
+    check_small(x, w, [0, 64, 136], ldy=256, what="ldy")
+
+
+def test_gemm_segments_with_very_different_scales():
+    rng = np.random.default_rng(301)
+    k = 256
+    x = bits_of(rng.standard_normal((96, k)))
+    w = bits_of(np.concatenate([rng.standard_normal((64, k)) * 1e-4, rng.standard_normal((32, k)) * 30.0,
+                                rng.standard_normal((160, k)) * 0.02]))
+    check_small(x, w, [0, 64, 96, 256], what="segment scales")
+
+
+def test_gemm_zero_activation_gives_zero():
+    rng = np.random.default_rng(302)
+    x = np.zeros((40, 64), dtype=np.uint16)
+    w = bits_of(rng.standard_normal((64, 64)))
+    y32, y16, aq, _ = run_gpu(x, w, [0, 64])
+    assert aq.g.item() == 0.0
+    assert torch.count_nonzero(y32).item() == 0
+
+
+def test_gemm_is_deterministic_and_stays_in_bounds():
+    rng = np.random.default_rng(303)
+    x, w = _xw(rng, 200, 160, 512)
+    aq = L.quantize_act(to_dev_bf16(x))
+    pw = L.pack_weight(to_dev_bf16(w), [0, 100, 160])
+    buf = torch.full((200 * 168 + 1024,), 12345.0, dtype=torch.float32, device="cuda")
+    y = buf[: 200 * 168].view(200, 168)[:, :160]
+    L.gemm(aq, pw, out=y)
+    first = y.clone()
+    for _ in range(3):
+        L.gemm(aq, pw, out=y)
+        assert torch.equal(y, first)
+    torch.cuda.synchronize()
+    pad = buf[: 200 * 168].view(200, 168)[:, 160:]
+    assert torch.all(pad == 12345.0) and torch.all(buf[200 * 168:] == 12345.0)
+
+
+def _sample_rows(m, rng):
+    rows = list(range(8)) + list(range(m - 8, m)) + list(rng.choice(np.arange(8, m - 8), 16, replace=False))
+    return np.array(sorted(set(rows)))
+
+
+@pytest.mark.parametrize("name", synth.CONFIG_ORDER)
+def test_gemm_full_workloads(name):
+    wl = workload(name)
+    cfg = wl["cfg"]
+    log("%s: GEMM on GPU" % name)
+    y32, y16, aq, pw = run_gpu(wl["x"], wl["w"], cfg.seg_offsets)
+    assert np.float32(aq.g.item()) == wl["gx"]
+    # BF16 output is the RNE of the FP32 output, everywhere.
+    assert torch.equal(y16.contiguous().view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
+    rows = _sample_rows(cfg.m, np.random.default_rng(cfg.index))
+    log("%s: oracle on %d sampled rows" % (name, len(rows)))
+    args = (wl["xp"], wl["xs"], wl["gx"], wl["wp"], wl["ws"], wl["gw"], cfg.seg_offsets)
+    y_ref = OG.gemm_f64(*args, rows=rows)
+    r_ref = OG.abs_bound(*args, rows=rows)
+    got = y32[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    rel = check_gemm(got, y_ref, r_ref, name)
+    log("%s: relative Frobenius error %.3g" % (name, rel))
