@@ -84,6 +84,32 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* 
   if (threadIdx.x == 0) partial[blockIdx.x] = __uint_as_float(mx << 16);
 }
 
+// Grid-strided loop over 16-element blocks: 32 bytes of bf16 in, 8 bytes of
+// packed codes and 1 scale byte out per block.
+template <bool kContig, bool kHuge>
+__device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, uint32_t n_blocks,
+                                                uint32_t blocks_per_row, uint32_t ldx,
+                                                uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                float g) {
+  const float gd6 = g * (1.0f / 6.0f);
+  const uint32_t stride = gridDim.x * kThreads;
+  for (uint32_t b = blockIdx.x * kThreads + threadIdx.x; b < n_blocks; b += stride) {
+    const uint4* src;
+    if (kContig) {
+      src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
+    } else {
+      uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
+      src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+    }
+    uint4 d0 = src[0], d1 = src[1];
+    uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    uint32_t c0, c1;
+    uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
+    reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
+    scales[b] = (uint8_t)sc;
+  }
+}
+
 template <bool kDynamic, bool kContig>
 __global__ __launch_bounds__(kThreads) void act_quant_kernel(
     const uint16_t* __restrict__ x, uint32_t n_blocks, uint32_t blocks_per_row, uint32_t ldx,
@@ -102,23 +128,10 @@ __global__ __launch_bounds__(kThreads) void act_quant_kernel(
   } else {
     g = *g_enc;
   }
-  const float gd6 = g * (1.0f / 6.0f);
-  const uint32_t stride = gridDim.x * kThreads;
-  for (uint32_t b = blockIdx.x * kThreads + threadIdx.x; b < n_blocks; b += stride) {
-    const uint4* src;
-    if (kContig) {
-      src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
-    } else {
-      uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
-      src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
-    }
-    uint4 d0 = src[0], d1 = src[1];
-    uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-    uint32_t c0, c1;
-    uint32_t sc = quantize_block(v, g, gd6, c0, c1);
-    reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
-    scales[b] = (uint8_t)sc;
-  }
+  if (g > kHugeScale)
+    quantize_blocks<kContig, true>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
+  else
+    quantize_blocks<kContig, false>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
 }
 
 __global__ void write_zero_scale_kernel(float* g_enc) { *g_enc = 0.0f; }

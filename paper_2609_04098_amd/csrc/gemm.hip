@@ -17,19 +17,32 @@
 // exactly 4 bytes of packed codes under one block scale; see packed_layout.h
 // for the index map shared by the activation and the prepacked weight.
 //
-// Tiling.  A workgroup of WM x WN waves computes a (WM*FM*32) x (WN*FN*32)
-// tile; each wave owns FM x FN accumulator fragments of 32 x 32 and decodes
-// its own FM + FN operand fragments per 16-deep step.  Operands are loaded
-// straight from global memory (L2) into registers with raw buffer loads,
-// one 64-deep chunk ahead of the MFMAs; out-of-range rows are clamped and the
-// buffer bounds return zeros past the end of each tensor.  Workgroups are
-// remapped so that each XCD (its own L2) runs a contiguous, M-grouped range
-// of tiles.
+// Two kernels:
+//  * gemm_lds_kernel (K % 64 == 0, N > 96): 256 threads, 256 x 128 tile,
+//    wave tile 128 x 64 (4 x 2 accumulator fragments, 128 registers) so
+//    that two workgroups share a CU and every SIMD runs two waves: with one
+//    wave per SIMD an MFMA stream stalls issue, and the decode VALU work of
+//    one wave hides behind the MFMAs of the other.  Raw packed operands move
+//    global -> LDS with direct-to-LDS buffer loads through a 4-stage ring
+//    (each fragment loaded once per workgroup); each wave reads its raw
+//    fragments of the next chunk from LDS while it decodes and multiplies the
+//    current one.  One barrier per 64-deep chunk.  The loop body is a single
+//    basic block in which MFMAs, decode VALU, LDS reads and the DMA issue of
+//    a later chunk are interleaved (sched_group_barrier), so that the vector
+//    memory queue and the VALU never stall the MFMA stream in bursts.
+//  * gemm_reg_kernel (any K % 16 == 0, and N <= 96): operands go straight
+//    from global memory to registers one chunk ahead; per-block masking of
+//    the scales handles a K tail.
+// Both remap workgroups so that each XCD (its own L2) runs a contiguous,
+// M-grouped range of tiles; out-of-range rows/columns read zeros through the
+// buffer bounds and are not stored.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "launch.h"
 #include "packed_layout.h"
+
+#define NVFP4_LDS __attribute__((address_space(3)))
 
 namespace nvfp4 {
 
@@ -39,12 +52,12 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef int int4v __attribute__((ext_vector_type(4)));
 
 constexpr int kNumXcd = 8;
-constexpr int kGroupM = 8;
+constexpr uint32_t kOOB = 0x80000000u;     // buffer offset past every tensor: loads return 0
 
 struct GemmParams {
   uint32_t M, N, K, ldy;
   uint32_t chunks;          // ceil(K / 64) chunks in the K loop
-  uint32_t w_kc, w_kg;      // packed-weight chunk and group counts
+  uint32_t w_kc;            // packed-weight chunk count (Kp / 64)
   uint32_t w_scale_offset;  // byte offset of the packed scale region
   uint32_t w_tiles;         // Np / 32
   uint32_t a_code_bytes, a_scale_bytes, w_bytes;
@@ -57,7 +70,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t b
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// E4M3 scale byte `sel` of a dword -> (S, S) in FP16 (exact: 4 significant
+// E4M3 scale byte kSel of a dword -> (S, S) in FP16 (exact: 4 significant
 // bits, 2^-9 <= S <= 448).
 template <int kSel>
 __device__ __forceinline__ half2v scale_pair(uint32_t bytes) {
@@ -81,6 +94,220 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Tile (tm, tn) of workgroup blockIdx.x: XCD-contiguous remap (workgroup i
+// runs on XCD i % 8), then M-grouped order (kGroupM tiles of M per group).
+template <int kGroupM>
+__device__ __forceinline__ void tile_of(const GemmParams& p, uint32_t& tm, uint32_t& tn) {
+  const uint32_t total = p.tiles_m * p.tiles_n;
+  const uint32_t pid0 = blockIdx.x;
+  const uint32_t xcd = pid0 % kNumXcd, per = total / kNumXcd, extra = total % kNumXcd;
+  const uint32_t pid = xcd * per + (xcd < extra ? xcd : extra) + pid0 / kNumXcd;
+  const uint32_t in_group = kGroupM * p.tiles_n;
+  const uint32_t first_m = (pid / in_group) * kGroupM;
+  const uint32_t gm = (p.tiles_m - first_m) < (uint32_t)kGroupM ? (p.tiles_m - first_m) : (uint32_t)kGroupM;
+  tm = first_m + (pid % in_group) % gm;
+  tn = (pid % in_group) / gm;
+}
+
+// Epilogue: y = acc / (G_A * G_W[s]) for the segment s of each column, BF16
+// (round to nearest even) or FP32, rows/columns beyond M/N not stored.
+template <int FM, int FN, bool kF32Out>
+__device__ __forceinline__ void store_tile(const floatx16 (&acc)[FM][FN], const GemmParams& p,
+                                           const float* __restrict__ a_g, const float* __restrict__ w_g,
+                                           void* __restrict__ y, uint32_t m0, uint32_t n0, uint32_t r,
+                                           uint32_t h) {
+  const float ga = *a_g;
+#pragma unroll
+  for (int fb = 0; fb < FN; ++fb) {
+    const uint32_t col = n0 + fb * 32 + r;
+    int s = 0;
+#pragma unroll
+    for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+    const float prod = ga * w_g[s];
+    const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+#pragma unroll
+    for (int fa = 0; fa < FM; ++fa) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
+        if (row < p.M && col < p.N) {
+          const float v = acc[fa][fb][i] * alpha;
+          if (kF32Out)
+            static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
+          else
+            static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ LDS path
+
+namespace lds {
+constexpr int WM = 2, WN = 2, FM = 4, FN = 2;
+constexpr int kThreads = WM * WN * 64;
+constexpr int BM = WM * FM * 32, BN = WN * FN * 32;        // 256 x 128
+constexpr int NFA = WM * FM, NFB = WN * FN;                 // 8 A and 4 B fragments per workgroup
+// One stage of the ring: raw codes (1 KB per fragment) and scales (256 B per
+// fragment: one dword per lane) of one 64-deep chunk.
+constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 256;
+constexpr int kStageBytes = kSB + NFB * 256;               // 15 KB
+constexpr int kStages = 4;
+constexpr int kLdsBytes = kStages * kStageBytes;           // 60 KB: two workgroups per CU
+constexpr int kLoadsPerWave = 6;                           // 2 A code + 2 A scale + 1 B code + 1 B scale
+constexpr int kGroupM = 4;
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits [3:0] and [15:14],
+// expcnt [6:4], lgkmcnt [11:8]; all-ones means "do not wait").
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitFirst = vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
+constexpr int kWaitNext = vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c+1 landed
+constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt(0)
+static_assert(NFA == 2 * WM * WN && NFB == WM * WN, "load assignment: 2 A and 1 B fragment per wave");
+}  // namespace lds
+
+template <bool kF32Out>
+__global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
+                                                                   const uint8_t* __restrict__ a_scales,
+                                                                   const float* __restrict__ a_g,
+                                                                   const uint8_t* __restrict__ w_packed,
+                                                                   const float* __restrict__ w_g,
+                                                                   void* __restrict__ y, GemmParams p) {
+  using namespace lds;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t r = lane & 31, h = lane >> 5;
+  uint32_t tm, tn;
+  tile_of<kGroupM>(p, tm, tn);
+  const uint32_t wm = wave / WN, wn = wave % WN;
+
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
+  const __amdgpu_buffer_rsrc_t rw = rsrc(w_packed, p.w_bytes);
+
+  // Wave w loads A fragments 2w, 2w+1 and B fragment w of every chunk.
+  uint32_t a_off[2], as_off[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t row = tm * BM + (2 * wave + i) * 32 + r;
+    a_off[i] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
+    as_off[i] = row < p.M ? row * (p.K >> 4) : kOOB;
+  }
+  const uint32_t nt = tn * (BN / 32) + wave;
+  const uint32_t b_off = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+  const uint32_t bs_off = nt < p.w_tiles ? p.w_scale_offset + nt * p.w_kc * 128u + r * 4u : kOOB;
+
+  // DMA of chunk kc into stage kc % kStages; chunks past the end read zeros.
+  auto issue = [&](uint32_t kc) {
+    uint8_t* st = smem + (kc % kStages) * kStageBytes;
+    const bool live = kc < p.chunks;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t f = 2 * wave + i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (NVFP4_LDS void*)(st + kA + f * 1024), 16,
+                                               (a_off[i] == kOOB || !live) ? kOOB : a_off[i] + kc * 32u, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)(st + kSA + f * 256), 4,
+                                               (as_off[i] == kOOB || !live) ? kOOB : as_off[i] + kc * 4u, 0, 0, 0);
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (NVFP4_LDS void*)(st + kB + wave * 1024), 16,
+                                             (b_off == kOOB || !live) ? kOOB : b_off + kc * 1024u, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (NVFP4_LDS void*)(st + kSB + wave * 256), 4,
+                                             (bs_off == kOOB || !live) ? kOOB : bs_off + kc * 128u, 0, 0, 0);
+  };
+
+  struct Regs {
+    int4v ca[FM], cb[FN];
+    uint32_t sa[FM], sb[FN];
+  };
+  auto read_stage = [&](Regs& R, uint32_t kc) {
+    const uint8_t* st = smem + (kc % kStages) * kStageBytes;
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
+      R.sa[f] = *(const uint32_t*)(st + kSA + (wm * FM + f) * 256 + lane * 4);
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
+      R.sb[f] = *(const uint32_t*)(st + kSB + (wn * FN + f) * 256 + lane * 4);
+    }
+  };
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx16{};
+
+#pragma unroll
+  for (int s = 0; s < kStages; ++s) issue(s);
+  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  __builtin_amdgcn_s_barrier();
+  Regs cur, nxt;
+  read_stage(cur, 0);
+
+  for (uint32_t c = 0; c < p.chunks; ++c) {
+    // cur is in registers, chunk c+1 has landed (loads are issued in
+    // order, and the last kStages-2 chunks may still be in flight); the
+    // barrier also guarantees every wave has read stage c % kStages.
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_waitcnt(kWaitNext);
+    __builtin_amdgcn_s_barrier();
+    issue(c + kStages);
+    read_stage(nxt, c + 1);
+
+    half2v sA[FM][2], sB[FN][2];
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      const uint32_t x = cur.sa[f] >> (16 * h);          // this lane's blocks 2h, 2h+1
+      sA[f][0] = scale_pair<0>(x);
+      sA[f][1] = scale_pair<1>(x);
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      const uint32_t x = cur.sb[f] >> (16 * h);
+      sB[f][0] = scale_pair<0>(x);
+      sB[f][1] = scale_pair<1>(x);
+    }
+    // Decode of step j+1 overlaps the MFMAs of step j.
+    half8 av[2][FM], bv[2][FN];
+#pragma unroll
+    for (int f = 0; f < FM; ++f) av[0][f] = decode8((uint32_t)cur.ca[f][0], sA[f][0]);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) bv[0][f] = decode8((uint32_t)cur.cb[f][0], sB[f][0]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = j & 1;
+      if (j < 3) {
+#pragma unroll
+        for (int f = 0; f < FM; ++f) av[u ^ 1][f] = decode8((uint32_t)cur.ca[f][j + 1], sA[f][(j + 1) >> 1]);
+#pragma unroll
+        for (int f = 0; f < FN; ++f) bv[u ^ 1][f] = decode8((uint32_t)cur.cb[f][j + 1], sB[f][(j + 1) >> 1]);
+      }
+#pragma unroll
+      for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+        for (int fb = 0; fb < FN; ++fb)
+          acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
+    }
+    // Schedule: every MFMA followed by 6 VALU; LDS reads of the next chunk
+    // and the DMA issue spread between the MFMAs.
+#pragma unroll
+    for (int i = 0; i < 4 * FM * FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);                       // VALU
+      if (i % 2 == 1 && i < 24) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+      if (i % 4 == 0 && i < 24) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM (DMA)
+    }
+    cur = nxt;
+  }
+  // Drain the DMA of the chunks past the end before the workgroup exits.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, tm * BM + wm * FM * 32, tn * BN + wn * FN * 32, r, h);
+}
+
+// ------------------------------------------------------------- register path
+
 // One 64-deep chunk of operands for a wave: FM activation fragments and FN
 // weight fragments, 16 code bytes and 2 scale bytes each per lane.
 template <int FM, int FN>
@@ -96,7 +323,7 @@ __device__ __forceinline__ void load_chunk(Chunk<FM, FN>& ch, uint32_t kc, const
                                            __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rs,
                                            __amdgpu_buffer_rsrc_t rw, const uint32_t (&a_row)[FM],
                                            const uint32_t (&b_tile)[FN], uint32_t lane) {
-  const uint32_t h = lane >> 5;
+  const uint32_t h = lane >> 5, r = lane & 31;
   const uint32_t kbq = p.K >> 4;                         // blocks per row
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
@@ -114,8 +341,8 @@ __device__ __forceinline__ void load_chunk(Chunk<FM, FN>& ch, uint32_t kc, const
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
     ch.b[f] = __builtin_amdgcn_raw_buffer_load_b128(rw, (b_tile[f] * p.w_kc + kc) * 1024u + lane * 16u, 0, 0);
-    const uint32_t soff = p.w_scale_offset + ((b_tile[f] * p.w_kg + (kc >> 2)) * 64u + lane) * 8u + (kc & 3u) * 2u;
-    ch.sb[f] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rw, soff, 0, 0);
+    const uint32_t soff = p.w_scale_offset + ((b_tile[f] * p.w_kc + kc) * 32u + r) * 4u;
+    ch.sb[f] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rw, soff, 0, 0) >> (16 * h);
   }
 }
 
@@ -142,27 +369,17 @@ __device__ __forceinline__ void mma_chunk(floatx16 (&acc)[FM][FN], const Chunk<F
 }
 
 template <int WM, int WN, int FM, int FN, bool kF32Out, bool kAlignedK>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const uint8_t* __restrict__ a_codes,
-                                                           const uint8_t* __restrict__ a_scales,
-                                                           const float* __restrict__ a_g,
-                                                           const uint8_t* __restrict__ w_packed,
-                                                           const float* __restrict__ w_g,
-                                                           void* __restrict__ y, GemmParams p) {
+__global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* __restrict__ a_codes,
+                                                               const uint8_t* __restrict__ a_scales,
+                                                               const float* __restrict__ a_g,
+                                                               const uint8_t* __restrict__ w_packed,
+                                                               const float* __restrict__ w_g,
+                                                               void* __restrict__ y, GemmParams p) {
   constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t r = lane & 31, h = lane >> 5;
-
-  // Tile index: XCD-contiguous remap, then M-grouped order.
-  const uint32_t total = p.tiles_m * p.tiles_n;
-  const uint32_t pid0 = blockIdx.x;
-  const uint32_t xcd = pid0 % kNumXcd, per = total / kNumXcd, extra = total % kNumXcd;
-  const uint32_t pid = xcd * per + (xcd < extra ? xcd : extra) + pid0 / kNumXcd;
-  const uint32_t in_group = kGroupM * p.tiles_n;
-  const uint32_t first_m = (pid / in_group) * kGroupM;
-  const uint32_t gm = (p.tiles_m - first_m) < (uint32_t)kGroupM ? (p.tiles_m - first_m) : (uint32_t)kGroupM;
-  const uint32_t tm = first_m + (pid % in_group) % gm;
-  const uint32_t tn = (pid % in_group) / gm;
-
+  uint32_t tm, tn;
+  tile_of<8>(p, tm, tn);
   const uint32_t wm = wave / WN, wn = wave % WN;
   const uint32_t m0 = tm * BM + wm * FM * 32, n0 = tn * BN + wn * FN * 32;
 
@@ -196,52 +413,41 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const uint8_t* __res
     cur = nxt;
   }
   mma_chunk<FM, FN>(acc, cur);
-
-  // Epilogue: y = acc / (G_A * G_W[s]) for the segment s of each column.
-  const float ga = *a_g;
-#pragma unroll
-  for (int fb = 0; fb < FN; ++fb) {
-    const uint32_t col = n0 + fb * 32 + r;
-    int s = 0;
-#pragma unroll
-    for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
-    const float prod = ga * w_g[s];
-    const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
-#pragma unroll
-    for (int fa = 0; fa < FM; ++fa) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
-        if (row < p.M && col < p.N) {
-          const float v = acc[fa][fb][i] * alpha;
-          if (kF32Out)
-            static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
-          else
-            static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
-        }
-      }
-    }
-  }
+  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, m0, n0, r, h);
 }
 
 template <int WM, int WN, int FM, int FN>
-static hipError_t launch_cfg(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
-                             const void* w_packed, const float* w_g, void* y, GemmParams p,
+static hipError_t launch_reg(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                             const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
                              bool out_f32, bool aligned, hipStream_t stream) {
   constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   p.tiles_m = (p.M + BM - 1) / BM;
   p.tiles_n = (p.N + BN - 1) / BN;
   const dim3 grid(p.tiles_m * p.tiles_n), block(WM * WN * 64);
-  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
-#define NVFP4_G(F32, AL)                                                                          \
-  hipLaunchKernelGGL((gemm_kernel<WM, WN, FM, FN, F32, AL>), grid, block, 0, stream, a_codes, a_scales, \
-                     a_g, wp, w_g, y, p)
+#define NVFP4_G(F32, AL)                                                                              \
+  hipLaunchKernelGGL((gemm_reg_kernel<WM, WN, FM, FN, F32, AL>), grid, block, 0, stream, a_codes, a_scales, \
+                     a_g, w_packed, w_g, y, p)
   if (out_f32) {
     if (aligned) NVFP4_G(true, true); else NVFP4_G(true, false);
   } else {
     if (aligned) NVFP4_G(false, true); else NVFP4_G(false, false);
   }
 #undef NVFP4_G
+  return hipGetLastError();
+}
+
+static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                             const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
+                             bool out_f32, hipStream_t stream) {
+  p.tiles_m = (p.M + lds::BM - 1) / lds::BM;
+  p.tiles_n = (p.N + lds::BN - 1) / lds::BN;
+  const dim3 grid(p.tiles_m * p.tiles_n), block(lds::kThreads);
+  if (out_f32)
+    hipLaunchKernelGGL(gemm_lds_kernel<true>, grid, block, lds::kLdsBytes, stream, a_codes, a_scales, a_g,
+                       w_packed, w_g, y, p);
+  else
+    hipLaunchKernelGGL(gemm_lds_kernel<false>, grid, block, lds::kLdsBytes, stream, a_codes, a_scales, a_g,
+                       w_packed, w_g, y, p);
   return hipGetLastError();
 }
 
@@ -258,7 +464,6 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   p.ldy = (uint32_t)ldy;
   p.chunks = (uint32_t)((K + 63) / 64);
   p.w_kc = (uint32_t)d.kc;
-  p.w_kg = (uint32_t)d.kg;
   p.w_scale_offset = (uint32_t)d.scale_offset;
   p.w_tiles = (uint32_t)(d.np / 32);
   p.a_code_bytes = (uint32_t)(M * K / 2);
@@ -267,10 +472,12 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   p.n_seg = n_seg;
   for (int i = 0; i < NVFP4_SEG_TABLE; ++i)
     p.seg_off[i] = (uint32_t)seg_offsets[i <= n_seg ? i : n_seg];
+  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   const bool aligned = (K % 64) == 0;
   if (N <= 96)
-    return launch_cfg<4, 1, 2, 3>(a_codes, a_scales, a_g, w_packed, w_g, y, p, out_f32, aligned, stream);
-  return launch_cfg<2, 2, 4, 4>(a_codes, a_scales, a_g, w_packed, w_g, y, p, out_f32, aligned, stream);
+    return launch_reg<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
+  if (aligned) return launch_lds(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+  return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }
 
 }  // namespace nvfp4

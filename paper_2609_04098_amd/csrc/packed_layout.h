@@ -2,7 +2,7 @@
 // and the GEMM.
 //
 // W has N rows (GEMM output columns) and K columns (reduction).  N is padded
-// to Np = 32 * ceil(N/32) and K to Kp = 256 * ceil(K/256); padding holds zero
+// to Np = 32 * ceil(N/32) and K to Kp = 64 * ceil(K/64); padding holds zero
 // codes and zero scales.  The GEMM reads W as the B operand of
 // v_mfma_f32_32x32x16_f16, one 32-column tile at a time.  In a 64-wide chunk
 // of K, lane l = 32 h + r of the wave handles output column r of the tile and
@@ -14,10 +14,12 @@
 //   codes:  [Np/32][Kp/64][64 lanes][16 bytes]; lane (h, r) of tile nt,
 //           chunk kc holds the canonical code bytes [kc*32 + 16 h, +16) of
 //           row 32 nt + r, i.e. blocks 4 kc + 2 h (bytes 0..7) and
-//           4 kc + 2 h + 1 (bytes 8..15).
-//   scales: at byte offset Np*Kp/2: [Np/32][Kp/256][64 lanes][8 bytes];
-//           byte 2 c + u of lane (h, r) in group kg is the E4M3 scale of
-//           block 16 kg + 4 c + 2 h + u of row 32 nt + r.
+//           4 kc + 2 h + 1 (bytes 8..15).  One wave-wide 16-byte load per
+//           tile and chunk, fully contiguous (1 KB).
+//   scales: at byte offset Np*Kp/2: [Np/32][Kp/64][32 rows][4 bytes]; the
+//           4 bytes of row r in tile nt, chunk kc are the E4M3 scales of
+//           blocks 4 kc .. 4 kc + 3 of row 32 nt + r (128 contiguous bytes
+//           per tile and chunk; lanes r and 32 + r read the same dword).
 #pragma once
 
 #include <stdint.h>
@@ -26,7 +28,7 @@ namespace nvfp4 {
 
 struct PackedDims {
   int64_t np, kp;          // padded N, padded K
-  int64_t kc, kg;          // chunks of 64 and groups of 256 along K
+  int64_t kc;              // chunks of 64 along K
   int64_t scale_offset;    // byte offset of the scale region
   int64_t bytes;           // total bytes
 };
@@ -34,9 +36,8 @@ struct PackedDims {
 inline PackedDims packed_dims(int64_t n, int64_t k) {
   PackedDims d;
   d.np = (n + 31) / 32 * 32;
-  d.kp = (k + 255) / 256 * 256;
+  d.kp = (k + 63) / 64 * 64;
   d.kc = d.kp / 64;
-  d.kg = d.kp / 256;
   d.scale_offset = d.np * d.kp / 2;
   d.bytes = d.scale_offset + d.np * d.kp / 16;
   return d;
@@ -50,9 +51,9 @@ __host__ __device__ inline uint32_t packed_code_offset(uint32_t n, uint32_t kb, 
 
 // Byte offset (from the start of the scale region) of the scale of block kb
 // of row n.
-__host__ __device__ inline uint32_t packed_scale_offset(uint32_t n, uint32_t kb, uint32_t kg_count) {
-  uint32_t nt = n >> 5, r = n & 31, kg = kb >> 4, c = (kb >> 2) & 3, h = (kb >> 1) & 1, u = kb & 1;
-  return ((nt * kg_count + kg) * 64u + h * 32u + r) * 8u + c * 2u + u;
+__host__ __device__ inline uint32_t packed_scale_offset(uint32_t n, uint32_t kb, uint32_t kc_count) {
+  uint32_t nt = n >> 5, r = n & 31, kc = kb >> 2, u = kb & 3;
+  return ((nt * kc_count + kc) * 32u + r) * 4u + u;
 }
 
 }  // namespace nvfp4

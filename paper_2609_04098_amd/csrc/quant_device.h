@@ -86,18 +86,22 @@ __device__ __forceinline__ float scale_value(uint32_t code) {
 
 struct ElemConsts {
   float g;      // G
-  float grq;    // ~ G / (S / 4)   (0 when S = 0)
+  float rq4;    // ~ 4 / S            (0 when S = 0)
+  float grq;    // ~ G / (S / 4)      (0 when S = 0; may overflow when G is huge)
   float sq;     // S / 4, exact
 };
+
+// G above this bound can make G * 4 / S overflow; such tensors (amax below
+// about 2^-89) take the two-multiply path.  The choice is per tensor, so it
+// is uniform across a launch.
+constexpr float kHugeScale = 0x1p100f;
 
 __device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
   ElemConsts c;
   c.g = g;
   c.sq = s * 0.25f;
-  // Clamped so that a saturated G (tensor amax below 2688 / FLT_MAX) cannot
-  // turn 0 * grq into NaN; any finite grq at least as large gives q >= 64
-  // for every non-zero |x|, which is the saturated code either way.
-  c.grq = s > 0.0f ? __builtin_fminf(g * (4.0f * __builtin_amdgcn_rcpf(s)), kFltMax) : 0.0f;
+  c.rq4 = s > 0.0f ? 4.0f * __builtin_amdgcn_rcpf(s) : 0.0f;
+  c.grq = g * c.rq4;
   return c;
 }
 
@@ -105,10 +109,12 @@ __device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
 // RNE_E2M1(|x| G / S) exactly (see the header comment): q = 4 |x| G / S is
 // compared with the integers 1, 3, 5, 7, 10, 14, 20 (four times the E2M1
 // midpoints).  q is clamped at 64, beyond every midpoint, so that a static
-// scale that overflows the range still saturates.
+// scale that overflows the range still saturates.  kHuge: q formed as
+// (|x| G) (4 / S), which cannot overflow into NaN when G is near FLT_MAX.
+template <bool kHuge>
 __device__ __forceinline__ float e2m1_arg(float x, const ElemConsts& c) {
   float ax = __builtin_fabsf(x);
-  float q = __builtin_fminf(ax * c.grq, 64.0f);
+  float q = __builtin_fminf(kHuge ? (ax * c.g) * c.rq4 : ax * c.grq, 64.0f);
   float n = __builtin_rintf(q);
   int s = sign3(__builtin_fmaf(ax, c.g, -(n * c.sq)));   // sign(|x| G - n S/4)
   uint32_t w = __float_as_uint(n) + (uint32_t)s;
@@ -118,24 +124,26 @@ __device__ __forceinline__ float e2m1_arg(float x, const ElemConsts& c) {
 // Packed codes of 8 elements (4 dwords of bf16 pairs); element 2j goes to
 // the low nibble of byte j.  The conversion divides by 2^exponent(4.0) = 4
 // and rounds to nearest even with saturation.
+template <bool kHuge>
 __device__ __forceinline__ uint32_t encode8(const uint32_t* d, const ElemConsts& k) {
   uint32_t r = 0u;
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[0]), k), e2m1_arg(bf16_hi(d[0]), k), 4.0f, 0);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[1]), k), e2m1_arg(bf16_hi(d[1]), k), 4.0f, 1);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[2]), k), e2m1_arg(bf16_hi(d[2]), k), 4.0f, 2);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg(bf16_lo(d[3]), k), e2m1_arg(bf16_hi(d[3]), k), 4.0f, 3);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[0]), k), e2m1_arg<kHuge>(bf16_hi(d[0]), k), 4.0f, 0);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[1]), k), e2m1_arg<kHuge>(bf16_hi(d[1]), k), 4.0f, 1);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[2]), k), e2m1_arg<kHuge>(bf16_hi(d[2]), k), 4.0f, 2);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[3]), k), e2m1_arg<kHuge>(bf16_hi(d[3]), k), 4.0f, 3);
   return r;
 }
 
 // Quantize one block: 8 dwords of bf16 pairs -> 2 dwords of packed codes;
 // returns the E4M3 scale code.
+template <bool kHuge>
 __device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g, float gd6,
                                                    uint32_t& c0, uint32_t& c1) {
   float amax_b = block_amax(v);
   uint32_t sc = scale_code(amax_b, g, gd6);
   ElemConsts k = elem_consts(g, scale_value(sc));
-  c0 = encode8(v, k);
-  c1 = encode8(v + 4, k);
+  c0 = encode8<kHuge>(v, k);
+  c1 = encode8<kHuge>(v + 4, k);
   return sc;
 }
 

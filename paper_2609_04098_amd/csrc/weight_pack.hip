@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kPackThreads) void seg_finalize_kernel(const float*
 __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __restrict__ w, uint32_t N,
                                                            uint32_t kb_valid, uint32_t ldw, uint32_t kb_pad,
                                                            uint32_t n_blocks_pad, uint32_t kc_count,
-                                                           uint32_t kg_count, SegTable segs,
+                                                           SegTable segs,
                                                            const float* __restrict__ g_enc_seg,
                                                            uint8_t* __restrict__ packed, uint32_t scale_offset) {
   for (uint32_t b = blockIdx.x * kPackThreads + threadIdx.x; b < n_blocks_pad; b += gridDim.x * kPackThreads) {
@@ -101,16 +101,17 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
       const uint4* src = reinterpret_cast<const uint4*>(w + (size_t)n * ldw) + 2 * kb;
       uint4 d0 = src[0], d1 = src[1];
       uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-      sc = quantize_block(v, g, g * (1.0f / 6.0f), c0, c1);
+      sc = g > kHugeScale ? quantize_block<true>(v, g, g * (1.0f / 6.0f), c0, c1)
+                          : quantize_block<false>(v, g, g * (1.0f / 6.0f), c0, c1);
     }
     *reinterpret_cast<uint2*>(packed + packed_code_offset(n, kb, kc_count)) = make_uint2(c0, c1);
-    packed[scale_offset + packed_scale_offset(n, kb, kg_count)] = (uint8_t)sc;
+    packed[scale_offset + packed_scale_offset(n, kb, kc_count)] = (uint8_t)sc;
   }
 }
 
 __global__ __launch_bounds__(kPackThreads) void unpack_kernel(const uint8_t* __restrict__ packed, uint32_t N,
                                                              uint32_t kb_valid, uint32_t kc_count,
-                                                             uint32_t kg_count, uint32_t scale_offset,
+                                                             uint32_t scale_offset,
                                                              uint8_t* __restrict__ codes,
                                                              uint8_t* __restrict__ scales) {
   const uint32_t n_blocks = N * kb_valid;
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(kPackThreads) void unpack_kernel(const uint8_t* __r
     uint32_t n = b / kb_valid, kb = b - n * kb_valid;
     uint2 c = *reinterpret_cast<const uint2*>(packed + packed_code_offset(n, kb, kc_count));
     reinterpret_cast<uint2*>(codes)[b] = c;
-    scales[b] = packed[scale_offset + packed_scale_offset(n, kb, kg_count)];
+    scales[b] = packed[scale_offset + packed_scale_offset(n, kb, kc_count)];
   }
 }
 
@@ -151,7 +152,7 @@ hipError_t launch_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
   const uint32_t n_blocks_pad = (uint32_t)(d.np * kb_pad);
   hipLaunchKernelGGL(pack_kernel, dim3(grid_cap(n_blocks_pad, 8192)), dim3(kPackThreads), 0, stream,
                      wp, (uint32_t)N, (uint32_t)(K / 16), (uint32_t)ldw, kb_pad, n_blocks_pad,
-                     (uint32_t)d.kc, (uint32_t)d.kg, segs, (const float*)g_enc_seg,
+                     (uint32_t)d.kc, segs, (const float*)g_enc_seg,
                      static_cast<uint8_t*>(packed), (uint32_t)d.scale_offset);
   return hipGetLastError();
 }
@@ -162,7 +163,7 @@ hipError_t launch_unpack_weight(const void* packed, int64_t N, int64_t K, uint8_
   const uint32_t kb_valid = (uint32_t)(K / 16);
   hipLaunchKernelGGL(unpack_kernel, dim3(grid_cap((uint64_t)N * kb_valid, 8192)), dim3(kPackThreads), 0,
                      stream, static_cast<const uint8_t*>(packed), (uint32_t)N, kb_valid, (uint32_t)d.kc,
-                     (uint32_t)d.kg, (uint32_t)d.scale_offset, codes, scales);
+                     (uint32_t)d.scale_offset, codes, scales);
   return hipGetLastError();
 }
 

@@ -43,9 +43,9 @@ def test_status_strings():
 def test_sizes():
     lib = C.lib()
     assert lib.nvfp4_quantize_act_workspace_bytes(8192, 5120) >= 4
-    # N padded to 32, K to 256: codes Np*Kp/2 + scales Np*Kp/16
+    # N padded to 32, K to 64: codes Np*Kp/2 + scales Np*Kp/16
     assert lib.nvfp4_packed_weight_bytes(96, 5120) == 96 * 5120 // 2 + 96 * 5120 // 16
-    assert lib.nvfp4_packed_weight_bytes(100, 80) == 128 * 256 // 2 + 128 * 256 // 16
+    assert lib.nvfp4_packed_weight_bytes(100, 80) == 128 * 128 // 2 + 128 * 128 // 16
     assert lib.nvfp4_packed_weight_bytes(0, 80) == 0
     assert lib.nvfp4_pack_weight_workspace_bytes(10, 32, 3) >= 3 * 4
 
