@@ -11,8 +11,10 @@
 //
 // Decode: v_cvt_scalef32_pk_f16_fp4 turns 2 packed codes into 2 FP16 values
 // (its scale operand only contributes a power of two, so it is left at 1.0)
-// and v_pk_mul_f16 multiplies the pair by the E4M3 block scale (converted
-// from its code with v_cvt_f32_fp8).  Lane l = 32 h + r of a wave supplies
+// and v_pk_mul_f16 multiplies the pair by the E4M3 block scale.  The LDS
+// kernel converts a lane's two scale codes per chunk with one
+// v_cvt_scalef32_pk_f16_fp8 and selects the half with op_sel; the register
+// kernel uses v_cvt_f32_fp8.  Lane l = 32 h + r of a wave supplies
 // row r of a 32-row fragment and 8 consecutive reduction indices, which is
 // exactly 4 bytes of packed codes under one block scale; see packed_layout.h
 // for the index map shared by the activation and the prepacked weight.
@@ -157,6 +159,7 @@ constexpr int kStages = 4;
 constexpr int kLdsBytes = kStages * kStageBytes;           // 60 KB: two workgroups per CU
 constexpr int kLoadsPerWave = 6;                           // 2 A code + 2 A scale + 1 B code + 1 B scale
 constexpr int kGroupM = 4;
+constexpr int kValuPerMfma = 5;                            // schedule: VALU slots after each MFMA
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits [3:0] and [15:14],
 // expcnt [6:4], lgkmcnt [11:8]; all-ones means "do not wait").
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -181,11 +184,9 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
   tile_of<kGroupM>(p, tm, tn);
   const uint32_t wm = wave / WN, wn = wave % WN;
 
-  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
-  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
-  const __amdgpu_buffer_rsrc_t rw = rsrc(w_packed, p.w_bytes);
-
-  // Wave w loads A fragments 2w, 2w+1 and B fragment w of every chunk.
+  // Per-lane offsets are fixed; the chunk advances the descriptors' base
+  // (and shrinks their size) in scalar registers.  Rows >= M and tiles past
+  // the packed weight get offsets beyond every descriptor: zeros.
   uint32_t a_off[2], as_off[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
@@ -195,24 +196,30 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
   }
   const uint32_t nt = tn * (BN / 32) + wave;
   const uint32_t b_off = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
-  const uint32_t bs_off = nt < p.w_tiles ? p.w_scale_offset + nt * p.w_kc * 128u + r * 4u : kOOB;
+  const uint32_t bs_off = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+  const uint8_t* w_scales = w_packed + p.w_scale_offset;
+  const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
 
+  auto chunk_rsrc = [&](const uint8_t* base, uint32_t bytes, uint32_t step, uint32_t kc) {
+    const uint32_t adv = kc * step;
+    const bool live = kc < p.chunks && adv < bytes;
+    return rsrc(base + (live ? adv : 0u), live ? bytes - adv : 0u);
+  };
   // DMA of chunk kc into stage kc % kStages; chunks past the end read zeros.
   auto issue = [&](uint32_t kc) {
     uint8_t* st = smem + (kc % kStages) * kStageBytes;
-    const bool live = kc < p.chunks;
+    const __amdgpu_buffer_rsrc_t ra = chunk_rsrc(a_codes, p.a_code_bytes, 32u, kc);
+    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(a_scales, p.a_scale_bytes, 4u, kc);
+    const __amdgpu_buffer_rsrc_t rb = chunk_rsrc(w_packed, p.w_scale_offset, 1024u, kc);
+    const __amdgpu_buffer_rsrc_t rbs = chunk_rsrc(w_scales, w_scale_bytes, 128u, kc);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const uint32_t f = 2 * wave + i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (NVFP4_LDS void*)(st + kA + f * 1024), 16,
-                                               (a_off[i] == kOOB || !live) ? kOOB : a_off[i] + kc * 32u, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)(st + kSA + f * 256), 4,
-                                               (as_off[i] == kOOB || !live) ? kOOB : as_off[i] + kc * 4u, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (NVFP4_LDS void*)(st + kA + f * 1024), 16, a_off[i], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)(st + kSA + f * 256), 4, as_off[i], 0, 0, 0);
     }
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (NVFP4_LDS void*)(st + kB + wave * 1024), 16,
-                                             (b_off == kOOB || !live) ? kOOB : b_off + kc * 1024u, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (NVFP4_LDS void*)(st + kSB + wave * 256), 4,
-                                             (bs_off == kOOB || !live) ? kOOB : bs_off + kc * 128u, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (NVFP4_LDS void*)(st + kB + wave * 1024), 16, b_off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs, (NVFP4_LDS void*)(st + kSB + wave * 256), 4, bs_off, 0, 0, 0);
   };
 
   struct Regs {
@@ -239,50 +246,36 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx16{};
 
-#pragma unroll
-  for (int s = 0; s < kStages; ++s) issue(s);
-  __builtin_amdgcn_s_waitcnt(kWaitFirst);
-  __builtin_amdgcn_s_barrier();
-  Regs cur, nxt;
-  read_stage(cur, 0);
-
-  for (uint32_t c = 0; c < p.chunks; ++c) {
-    // cur is in registers, chunk c+1 has landed (loads are issued in
-    // order, and the last kStages-2 chunks may still be in flight); the
-    // barrier also guarantees every wave has read stage c % kStages.
+  // One chunk: wait, barrier, DMA of chunk c + kStages, LDS reads of chunk
+  // c+1 into `next`, decode + MFMA of `cur`.
+  auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_waitcnt(kWaitNext);
     __builtin_amdgcn_s_barrier();
     issue(c + kStages);
-    read_stage(nxt, c + 1);
-
-    half2v sA[FM][2], sB[FN][2];
+    read_stage(next, c + 1);
+    // Both block scales of the lane (blocks 2h, 2h+1 of the chunk) as FP16.
+    half2v sA[FM], sB[FN];
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      const uint32_t x = cur.sa[f] >> (16 * h);          // this lane's blocks 2h, 2h+1
-      sA[f][0] = scale_pair<0>(x);
-      sA[f][1] = scale_pair<1>(x);
-    }
+    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sa[f] >> (16 * h), 1.0f, false);
 #pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      const uint32_t x = cur.sb[f] >> (16 * h);
-      sB[f][0] = scale_pair<0>(x);
-      sB[f][1] = scale_pair<1>(x);
-    }
-    // Decode of step j+1 overlaps the MFMAs of step j.
+    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sb[f] >> (16 * h), 1.0f, false);
     half8 av[2][FM], bv[2][FN];
 #pragma unroll
-    for (int f = 0; f < FM; ++f) av[0][f] = decode8((uint32_t)cur.ca[f][0], sA[f][0]);
+    for (int f = 0; f < FM; ++f) av[0][f] = decode8((uint32_t)cur.ca[f][0], __builtin_shufflevector(sA[f], sA[f], 0, 0));
 #pragma unroll
-    for (int f = 0; f < FN; ++f) bv[0][f] = decode8((uint32_t)cur.cb[f][0], sB[f][0]);
+    for (int f = 0; f < FN; ++f) bv[0][f] = decode8((uint32_t)cur.cb[f][0], __builtin_shufflevector(sB[f], sB[f], 0, 0));
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int u = j & 1;
       if (j < 3) {
+        const int t = (j + 1) >> 1;
 #pragma unroll
-        for (int f = 0; f < FM; ++f) av[u ^ 1][f] = decode8((uint32_t)cur.ca[f][j + 1], sA[f][(j + 1) >> 1]);
+        for (int f = 0; f < FM; ++f)
+          av[u ^ 1][f] = decode8((uint32_t)cur.ca[f][j + 1], t ? __builtin_shufflevector(sA[f], sA[f], 1, 1) : __builtin_shufflevector(sA[f], sA[f], 0, 0));
 #pragma unroll
-        for (int f = 0; f < FN; ++f) bv[u ^ 1][f] = decode8((uint32_t)cur.cb[f][j + 1], sB[f][(j + 1) >> 1]);
+        for (int f = 0; f < FN; ++f)
+          bv[u ^ 1][f] = decode8((uint32_t)cur.cb[f][j + 1], t ? __builtin_shufflevector(sB[f], sB[f], 1, 1) : __builtin_shufflevector(sB[f], sB[f], 0, 0));
       }
 #pragma unroll
       for (int fa = 0; fa < FM; ++fa)
@@ -290,15 +283,23 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
         for (int fb = 0; fb < FN; ++fb)
           acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
     }
-    // Schedule: every MFMA followed by 6 VALU; LDS reads of the next chunk
-    // and the DMA issue spread between the MFMAs.
 #pragma unroll
     for (int i = 0; i < 4 * FM * FN; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);                       // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);            // VALU
       if (i % 2 == 1 && i < 24) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
       if (i % 4 == 0 && i < 24) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM (DMA)
     }
+  };
+
+#pragma unroll
+  for (int s = 0; s < kStages; ++s) issue(s);
+  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  __builtin_amdgcn_s_barrier();
+  Regs cur, nxt;
+  read_stage(cur, 0);
+  for (uint32_t c = 0; c < p.chunks; ++c) {
+    step(c, cur, nxt);
     cur = nxt;
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
