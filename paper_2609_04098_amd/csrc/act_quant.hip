@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* 
 
 // Grid-strided loop over 16-element blocks: 32 bytes of bf16 in, 8 bytes of
 // packed codes and 1 scale byte out per block.
-template <bool kContig, bool kHuge>
+template <bool kContig, bool kHuge, bool kClamp>
 __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, uint32_t n_blocks,
                                                 uint32_t blocks_per_row, uint32_t ldx,
                                                 uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -104,7 +104,7 @@ __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, 
     uint4 d0 = src[0], d1 = src[1];
     uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
     uint32_t c0, c1;
-    uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
+    uint32_t sc = quantize_block<kHuge, kClamp>(v, g, gd6, c0, c1);
     reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
     scales[b] = (uint8_t)sc;
   }
@@ -128,10 +128,11 @@ __global__ __launch_bounds__(kThreads) void act_quant_kernel(
   } else {
     g = *g_enc;
   }
+  // A dynamic G bounds |q| by 36; a static G needs the clamp.
   if (g > kHugeScale)
-    quantize_blocks<kContig, true>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
+    quantize_blocks<kContig, true, !kDynamic>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
   else
-    quantize_blocks<kContig, false>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
+    quantize_blocks<kContig, false, !kDynamic>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
 }
 
 __global__ void write_zero_scale_kernel(float* g_enc) { *g_enc = 0.0f; }

@@ -34,10 +34,14 @@ __device__ __forceinline__ float bf16_lo(uint32_t d) { return __uint_as_float(d 
 __device__ __forceinline__ float bf16_hi(uint32_t d) { return __uint_as_float(d & 0xFFFF0000u); }
 
 __device__ __forceinline__ int sign3(float e) {
-  // -1, 0, +1 for e < 0, e == +0, e > 0 (e is never -0.0 here: an exact
-  // zero from fma is +0 under round-to-nearest-even).  NaN maps to +-1.
-  int b = (int)__float_as_uint(e);
-  return b < -1 ? -1 : (b > 1 ? 1 : b);
+  // -1, 0, +1 for e < 0, e == +0, e > 0 as one v_med3_i32 on the bit
+  // pattern (e is never -0.0 here: an exact zero from fma is +0 under
+  // round-to-nearest-even).  NaN maps to +-1.
+  // (The compiler lowers min/max here to compares and selects, so the
+  // instruction is written directly.)
+  int r;
+  asm("v_med3_i32 %0, %1, -1, 1" : "=v"(r) : "v"(__float_as_uint(e)));
+  return r;
 }
 
 // Per-tensor global scale G = fl32(2688 / amax); 0 for amax = 0; overflow
@@ -105,45 +109,51 @@ __device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
   return c;
 }
 
-// Binary32 value w with the sign of x such that RNE_E2M1(w / 4) equals
-// RNE_E2M1(|x| G / S) exactly (see the header comment): q = 4 |x| G / S is
-// compared with the integers 1, 3, 5, 7, 10, 14, 20 (four times the E2M1
-// midpoints).  q is clamped at 64, beyond every midpoint, so that a static
-// scale that overflows the range still saturates.  kHuge: q formed as
-// (|x| G) (4 / S), which cannot overflow into NaN when G is near FLT_MAX.
-template <bool kHuge>
+// Binary32 value w such that RNE_E2M1(w / 4) equals sign(x) RNE_E2M1(|x| G / S)
+// exactly (see the header comment).  q = 4 x G / S keeps the sign of x;
+// n = rint(q) is the only integer that can lie between q and its
+// approximation, and the thresholds 1, 3, 5, 7, 10, 14, 20 (four times the
+// E2M1 midpoints) are integers.  e = |x| G - |n| S / 4, rounded once by the
+// fma (abs/neg are free source modifiers), has the exact sign of |q| - |n|;
+// adding that sign to the bit pattern of n moves |n| by one ulp towards |q|
+// (for n = +-0, e >= 0).  The sign of x rides along in n, including -0.0.
+// kClamp (static scales): q is clamped to [-64, 64], beyond every midpoint,
+// so that an input beyond the calibrated range still saturates; with a
+// dynamic scale |q| <= 36 holds by construction.  kHuge: q formed as
+// (x G) (4 / S), which cannot overflow when G is near FLT_MAX.
+template <bool kHuge, bool kClamp>
 __device__ __forceinline__ float e2m1_arg(float x, const ElemConsts& c) {
-  float ax = __builtin_fabsf(x);
-  float q = __builtin_fminf(kHuge ? (ax * c.g) * c.rq4 : ax * c.grq, 64.0f);
+  float q = kHuge ? (x * c.g) * c.rq4 : x * c.grq;
+  if (kClamp) q = __builtin_amdgcn_fmed3f(q, -64.0f, 64.0f);
   float n = __builtin_rintf(q);
-  int s = sign3(__builtin_fmaf(ax, c.g, -(n * c.sq)));   // sign(|x| G - n S/4)
-  uint32_t w = __float_as_uint(n) + (uint32_t)s;
-  return __uint_as_float(w | (__float_as_uint(x) & 0x80000000u));
+  float t = n * c.sq;                                          // exact
+  int s = sign3(__builtin_fmaf(__builtin_fabsf(x), c.g, -__builtin_fabsf(t)));
+  return __uint_as_float(__float_as_uint(n) + (uint32_t)s);
 }
 
 // Packed codes of 8 elements (4 dwords of bf16 pairs); element 2j goes to
 // the low nibble of byte j.  The conversion divides by 2^exponent(4.0) = 4
 // and rounds to nearest even with saturation.
-template <bool kHuge>
+template <bool kHuge, bool kClamp>
 __device__ __forceinline__ uint32_t encode8(const uint32_t* d, const ElemConsts& k) {
   uint32_t r = 0u;
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[0]), k), e2m1_arg<kHuge>(bf16_hi(d[0]), k), 4.0f, 0);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[1]), k), e2m1_arg<kHuge>(bf16_hi(d[1]), k), 4.0f, 1);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[2]), k), e2m1_arg<kHuge>(bf16_hi(d[2]), k), 4.0f, 2);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(bf16_lo(d[3]), k), e2m1_arg<kHuge>(bf16_hi(d[3]), k), 4.0f, 3);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[0]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[0]), k), 4.0f, 0);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[1]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[1]), k), 4.0f, 1);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[2]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[2]), k), 4.0f, 2);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[3]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[3]), k), 4.0f, 3);
   return r;
 }
 
 // Quantize one block: 8 dwords of bf16 pairs -> 2 dwords of packed codes;
 // returns the E4M3 scale code.
-template <bool kHuge>
+template <bool kHuge, bool kClamp>
 __device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g, float gd6,
                                                    uint32_t& c0, uint32_t& c1) {
   float amax_b = block_amax(v);
   uint32_t sc = scale_code(amax_b, g, gd6);
   ElemConsts k = elem_consts(g, scale_value(sc));
-  c0 = encode8<kHuge>(v, k);
-  c1 = encode8<kHuge>(v + 4, k);
+  c0 = encode8<kHuge, kClamp>(v, k);
+  c1 = encode8<kHuge, kClamp>(v + 4, k);
   return sc;
 }
 
