@@ -18,6 +18,8 @@ vs. fused-GEMM scaling"):
   output segment scaled by its own global scales (the per-module scales of
   section 6), an exact int64 form of the same sum, and the sum of |a_k b_k|
   used by the tolerance.
+* ``harmonize`` the repair of section 6 for a fused weight group: one shared
+  global scale with the ratio folded into re-rounded E4M3 block scales.
 * ``stats``    block statistics of Table 2 (max/RMS, kurtosis, one-hot blocks,
   relative quantization error), used only as sanity bands for synthetic data.
 
@@ -26,4 +28,4 @@ every product that is compared, see ``quant``), so codes and scales are a
 function of the inputs alone, independent of any operation order.
 """
 
-from . import formats, quant, gemm, stats  # noqa: F401
+from . import formats, quant, gemm, harmonize, stats  # noqa: F401
