@@ -188,7 +188,25 @@ def main():
     gemm_tflops = flops / (gemm_avg * 1e-3) / 1e12
     aq_bytes = cfg.m * cfg.k * (2 + 0.5 + 1.0 / 16)
     aq_gbs = aq_bytes / (aq_avg * 1e-3) / 1e9
-    traffic = committed_traffic()
+    traffic = committed_traffic() if cfg.name == WORKLOAD else None
+    gemm_bytes = (cfg.m + cfg.n) * cfg.k * (0.5 + 1.0 / 16) + 2.0 * cfg.m * cfg.n
+    gemm_gbs = gemm_bytes / (gemm_avg * 1e-3) / 1e9
+
+    # Static-scale act-quant (a calibrated G, here the dynamic one just
+    # computed): one pass over X.  Timed inside [act-quant, GEMM] steps so X
+    # comes from HBM as in the dynamic steps.
+    def quantize_static():
+        C.nvfp4_quantize_act(x, aq.codes, aq.scales, aq.g, C.NVFP4_STATIC, None, stream)
+
+    st_events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        st_events[i][0].record(stream)
+        quantize_static()
+        st_events[i][1].record(stream)
+        L.gemm(aq, pw, out=y)
+    torch.cuda.synchronize()
+    aq_static_avg = float(np.mean([e[0].elapsed_time(e[1]) for e in st_events]))
+    aq_static_gbs = aq_bytes / (aq_static_avg * 1e-3) / 1e9
     log("step %.3f ms (events %.3f), act-quant %.3f ms, GEMM %.3f ms" % (
         ms_per_step, float(np.mean(step_ms)), aq_avg, gemm_avg))
 
@@ -214,7 +232,8 @@ def main():
         "pct_of_mfma_peak": round(100.0 * value / MFMA_F16_PEAK_TFLOPS, 2),
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm_lds_kernel<false> (NVFP4 GEMM + segment-scaled bf16 epilogue)",
+            "kernel": ("gemm_splitk_kernel<4, 2, 3> (tall-skinny NVFP4 GEMM + segment-scaled bf16 epilogue)"
+                       if cfg.n <= 96 else "gemm_lds_kernel<false> (NVFP4 GEMM + segment-scaled bf16 epilogue)"),
             "achieved": round(gemm_tflops, 2),
             "peak": MFMA_F16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
@@ -222,11 +241,18 @@ def main():
             "traffic": traffic,
             "algorithmic_flops_per_launch": flops,
             "avg_launch_ms": round(gemm_avg, 4),
+            "hbm": {"algorithmic_bytes": gemm_bytes, "achieved": round(gemm_gbs, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(gemm_gbs / HBM_PEAK_GBS, 4)},
         },
         "act_quant": {
             "bound": "hbm", "avg_ms": round(aq_avg, 4), "achieved": round(aq_gbs, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(aq_gbs / HBM_PEAK_GBS, 4),
             "algorithmic_bytes": aq_bytes,
+        },
+        "act_quant_static": {
+            "bound": "hbm", "avg_ms": round(aq_static_avg, 4), "achieved": round(aq_static_gbs, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(aq_static_gbs / HBM_PEAK_GBS, 4),
+            "note": "one pass with a given (calibrated) global scale; not part of value",
         },
         "frac_of_mxfp4_peak": round(value / MXFP4_PEAK_TFLOPS, 4),
         "prepack_ms": round(prepack_ms, 3),

@@ -105,7 +105,7 @@ int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
- * tile layout of the codes and block scales, N padded to 32 and K to 256. */
+ * tile layout of the codes and block scales, N padded to 32 and K to 64. */
 size_t nvfp4_packed_weight_bytes(int64_t N, int64_t K);
 
 /* Workspace bytes nvfp4_pack_weight needs (per-segment partial maxima). */
@@ -141,6 +141,31 @@ int nvfp4_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
  */
 int nvfp4_unpack_weight(const void* packed, int64_t N, int64_t K,
                         uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
+ * Global-scale harmonization of a fused weight group (paper, section 6,
+ * "Per-module calibration vs. fused-GEMM scaling": the checkpoint-side
+ * repair that lets one global scale serve several per-module-calibrated
+ * segments).  Rewrites a packed weight IN PLACE so that the whole group uses
+ * one shared global scale:
+ *   G_shared = the smallest G_s > 0 (the scale of the segment with the
+ *              largest amax; 0 if every G_s is 0),
+ *   every block scale S of segment s becomes RNE_E4M3(S * G_shared / G_s)
+ *   (one round-to-nearest-even of the exact value, ties to the even code,
+ *   E4M3 subnormals kept; segments with G_s = 0 or G_s = G_shared are left
+ *   as they are).  The E2M1 codes do not change.  Afterwards call nvfp4_gemm
+ *   with one segment [0, N] and w_g_enc_seg = g_shared.
+ *
+ *   packed       in/out, a packed weight for this N and K.
+ *   seg_offsets  HOST array, as for nvfp4_pack_weight.
+ *   g_enc_seg    device float [n_seg]: the segments' G_s (read only).
+ *   g_shared     out, device float: G_shared; must not lie inside g_enc_seg.
+ * Requirements: as for nvfp4_unpack_weight; valid segments.
+ * Errors: NVFP4_EINVAL, NVFP4_EUNSUPPORTED, NVFP4_EHIP.
+ */
+int nvfp4_harmonize_weight(void* packed, int64_t N, int64_t K,
+                           const int64_t* seg_offsets, int n_seg,
+                           const float* g_enc_seg, float* g_shared, void* stream);
 
 /*
  * NVFP4 x NVFP4 GEMM with FP32 accumulation and a per-segment scaled

@@ -159,6 +159,23 @@ int nvfp4_unpack_weight(const void* packed, int64_t N, int64_t K, uint8_t* codes
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 
+int nvfp4_harmonize_weight(void* packed, int64_t N, int64_t K, const int64_t* seg_offsets, int n_seg,
+                           const float* g_enc_seg, float* g_shared, void* stream) {
+  if (N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
+  if (nvfp4::packed_dims(N, K).bytes >= kI32Lim) return NVFP4_EINVAL;
+  if (!valid_segments(seg_offsets, n_seg, N)) return NVFP4_EINVAL;
+  if (packed == nullptr || g_enc_seg == nullptr || g_shared == nullptr) return NVFP4_EINVAL;
+  if (!aligned16(packed) || (reinterpret_cast<uintptr_t>(g_enc_seg) & 3u) ||
+      (reinterpret_cast<uintptr_t>(g_shared) & 3u))
+    return NVFP4_EINVAL;
+  if (g_shared >= g_enc_seg && g_shared < g_enc_seg + n_seg) return NVFP4_EINVAL;
+  int st = check_device();
+  if (st != NVFP4_OK) return st;
+  hipError_t e = nvfp4::launch_harmonize_weight(packed, N, K, seg_offsets, n_seg, g_enc_seg, g_shared,
+                                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
 int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
                int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
                const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype, void* stream) {

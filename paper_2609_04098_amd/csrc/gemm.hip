@@ -32,9 +32,14 @@
 //    basic block in which MFMAs, decode VALU, LDS reads and the DMA issue of
 //    a later chunk are interleaved (sched_group_barrier), so that the vector
 //    memory queue and the VALU never stall the MFMA stream in bursts.
-//  * gemm_reg_kernel (any K % 16 == 0, and N <= 96): operands go straight
-//    from global memory to registers one chunk ahead; per-block masking of
-//    the scales handles a K tail.
+//  * gemm_splitk_kernel (N <= 96, the tall-skinny gate projections): the
+//    output has too few 32 x 32 tiles for two waves per SIMD, so the four
+//    waves of a workgroup share one 64 x 96 tile and split its reduction;
+//    operands go straight from global memory to registers, three chunks in
+//    flight per wave, and the partial sums meet in LDS.
+//  * gemm_reg_kernel (K % 64 != 0, N > 96): operands go straight from global
+//    memory to registers one chunk ahead; per-block masking of the scales
+//    handles a K tail.
 // Both remap workgroups so that each XCD (its own L2) runs a contiguous,
 // M-grouped range of tiles; out-of-range rows/columns read zeros through the
 // buffer bounds and are not stored.
@@ -315,8 +320,11 @@ template <int FM, int FN>
 struct Chunk {
   int4v a[FM];
   int4v b[FN];
-  uint32_t sa[FM];   // low 2 bytes: scales of blocks 4 kc + 2h + {0, 1}
-  uint32_t sb[FN];
+  // Scales of blocks 4 kc + 2h + {0, 1} (bytes 0 and 1).  Kept as loaded:
+  // any widening is left to the consumer, so that no instruction right after
+  // the loads waits for them.
+  uint16_t sa[FM];
+  uint16_t sb[FN];
 };
 
 template <int FM, int FN, bool kAlignedK>
@@ -332,18 +340,18 @@ __device__ __forceinline__ void load_chunk(Chunk<FM, FN>& ch, uint32_t kc, const
     const uint32_t blk = kc * 4u + 2u * h;
     const uint32_t soff = a_row[f] * kbq + blk;
     if (kAlignedK) {
-      ch.sa[f] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, soff, 0, 0);
+      ch.sa[f] = __builtin_amdgcn_raw_buffer_load_b16(rs, soff, 0, 0);
     } else {
       uint32_t s0 = blk < kbq ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(rs, soff, 0, 0) : 0u;
       uint32_t s1 = blk + 1 < kbq ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(rs, soff + 1, 0, 0) : 0u;
-      ch.sa[f] = (s0 & 0xFFu) | ((s1 & 0xFFu) << 8);
+      ch.sa[f] = (uint16_t)((s0 & 0xFFu) | ((s1 & 0xFFu) << 8));
     }
   }
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
     ch.b[f] = __builtin_amdgcn_raw_buffer_load_b128(rw, (b_tile[f] * p.w_kc + kc) * 1024u + lane * 16u, 0, 0);
-    const uint32_t soff = p.w_scale_offset + ((b_tile[f] * p.w_kc + kc) * 32u + r) * 4u;
-    ch.sb[f] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rw, soff, 0, 0) >> (16 * h);
+    const uint32_t soff = p.w_scale_offset + ((b_tile[f] * p.w_kc + kc) * 32u + r) * 4u + 2u * h;
+    ch.sb[f] = __builtin_amdgcn_raw_buffer_load_b16(rw, soff, 0, 0);
   }
 }
 
@@ -417,6 +425,132 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
   store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, m0, n0, r, h);
 }
 
+// Tall-skinny shapes (N <= 96): the output has too few 32 x 32 tiles to give
+// every SIMD two waves, so the KS waves of a workgroup share one FM x FN
+// fragment tile and split its reduction: wave w takes chunks w, w + KS, ...
+// (adjacent chunks of a row are read by adjacent waves at the same time).
+// The partial sums meet in LDS; fragment f is summed (in wave order, so the
+// result is deterministic) and stored by wave f % KS.
+template <int KS, int FM, int FN, int kDepth, bool kF32Out, bool kAlignedK>
+__global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* __restrict__ a_codes,
+                                                             const uint8_t* __restrict__ a_scales,
+                                                             const float* __restrict__ a_g,
+                                                             const uint8_t* __restrict__ w_packed,
+                                                             const float* __restrict__ w_g,
+                                                             void* __restrict__ y, GemmParams p) {
+  constexpr int BM = FM * 32, BN = FN * 32;
+  __shared__ floatx16 part[KS][64];
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t r = lane & 31, h = lane >> 5;
+  uint32_t tm, tn;
+  tile_of<8>(p, tm, tn);
+  const uint32_t m0 = tm * BM, n0 = tn * BN;
+
+  uint32_t a_row[FM], b_tile[FN];
+#pragma unroll
+  for (int f = 0; f < FM; ++f) {
+    uint32_t row = m0 + f * 32 + r;
+    a_row[f] = row < p.M ? row : p.M - 1;
+  }
+#pragma unroll
+  for (int f = 0; f < FN; ++f) {
+    uint32_t t = (n0 >> 5) + f;
+    b_tile[f] = t < p.w_tiles ? t : p.w_tiles - 1;
+  }
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
+  const __amdgpu_buffer_rsrc_t rw = rsrc(w_packed, p.w_bytes);
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+    for (int fb = 0; fb < FN; ++fb) acc[fa][fb] = floatx16{};
+
+  // kDepth chunks of this wave in flight: buffer d holds the wave's chunk
+  // i while the loads of its next kDepth - 1 chunks are outstanding.  The
+  // loads are unconditional (a prefetch past the wave's last chunk re-reads
+  // the last chunk of the row) so that the loop body is one basic block and
+  // the memory counter waits only for the chunk about to be used.
+  const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+  auto kc_of = [&](uint32_t i) -> uint32_t {
+    const uint32_t kc = wave + KS * i;
+    return kc < p.chunks ? kc : p.chunks - 1;
+  };
+  Chunk<FM, FN> buf[kDepth];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) load_chunk<FM, FN, kAlignedK>(buf[d], kc_of(d), p, ra, rs, rw, a_row, b_tile, lane);
+  uint32_t i = 0;
+  for (; i + kDepth <= n_mine; i += kDepth) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      mma_chunk<FM, FN>(acc, buf[d]);
+      // Issue the refill here: left to itself the scheduler sinks the loads
+      // to the end of the body and the prefetch distance is lost.
+      __builtin_amdgcn_sched_barrier(0);
+      load_chunk<FM, FN, kAlignedK>(buf[d], kc_of(i + d + kDepth), p, ra, rs, rw, a_row, b_tile, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < kDepth - 1; ++d)
+    if (i + d < n_mine) mma_chunk<FM, FN>(acc, buf[d]);
+
+  const float ga = *a_g;
+#pragma unroll
+  for (int fa = 0; fa < FM; ++fa) {
+#pragma unroll
+    for (int fb = 0; fb < FN; ++fb) {
+      const uint32_t owner = (fa * FN + fb) % KS;
+      part[wave][lane] = acc[fa][fb];
+      __syncthreads();
+      if (wave == owner) {
+        floatx16 sum = part[0][lane];
+#pragma unroll
+        for (int w = 1; w < KS; ++w) sum += part[w][lane];
+        const uint32_t col = n0 + fb * 32 + r;
+        int s = 0;
+#pragma unroll
+        for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+        const float prod = ga * w_g[s];
+        const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
+          if (row < p.M && col < p.N) {
+            const float v = sum[i] * alpha;
+            if (kF32Out)
+              static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
+            else
+              static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+template <int KS, int FM, int FN, int kDepth>
+static hipError_t launch_splitk(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                                const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
+                                bool out_f32, bool aligned, hipStream_t stream) {
+  constexpr int BM = FM * 32, BN = FN * 32;
+  p.tiles_m = (p.M + BM - 1) / BM;
+  p.tiles_n = (p.N + BN - 1) / BN;
+  const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
+#define NVFP4_G(F32, AL)                                                                               \
+  hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kDepth, F32, AL>), grid, block, 0, stream, a_codes, a_scales, \
+                     a_g, w_packed, w_g, y, p)
+  if (out_f32) {
+    if (aligned) NVFP4_G(true, true); else NVFP4_G(true, false);
+  } else {
+    if (aligned) NVFP4_G(false, true); else NVFP4_G(false, false);
+  }
+#undef NVFP4_G
+  return hipGetLastError();
+}
+
 template <int WM, int WN, int FM, int FN>
 static hipError_t launch_reg(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                              const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
@@ -476,7 +610,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   const bool aligned = (K % 64) == 0;
   if (N <= 96)
-    return launch_reg<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
+    return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
   if (aligned) return launch_lds(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }

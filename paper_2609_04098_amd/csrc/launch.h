@@ -28,6 +28,10 @@ hipError_t launch_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
 hipError_t launch_unpack_weight(const void* packed, int64_t N, int64_t K, uint8_t* codes,
                                 uint8_t* scales, hipStream_t stream);
 
+hipError_t launch_harmonize_weight(void* packed, int64_t N, int64_t K, const int64_t* seg_offsets,
+                                   int n_seg, const float* g_enc_seg, float* g_shared,
+                                   hipStream_t stream);
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                        int64_t M, int64_t K, const void* w_packed, int64_t N,
                        const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,

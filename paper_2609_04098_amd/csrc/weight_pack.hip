@@ -125,6 +125,62 @@ __global__ __launch_bounds__(kPackThreads) void unpack_kernel(const uint8_t* __r
   }
 }
 
+// ------------------------------------------------- fused-group harmonization
+//
+// Paper, section 6 ("Per-module calibration vs. fused-GEMM scaling"): the
+// segments of a fused weight are rewritten to one shared global scale, the
+// smallest positive encode-direction G_s (the largest-amax segment's), and
+// each block scale S of segment s becomes RNE_E4M3(S * G_shared / G_s); the
+// E2M1 codes stay.  This is an offline rewrite, so it decides in float64,
+// where every compared product is exact: S * G_shared has at most 4 + 24
+// significant bits, (v_c + v_c+1) * G_s at most 5 + 24.
+
+// Value of a non-negative E4M3 code (0..126) in float64, exactly.
+__device__ __forceinline__ double e4m3_f64(uint32_t c) {
+  const uint32_t e = c >> 3, m = c & 7u;
+  if (e == 0) return (double)m * 0x1p-9;
+  return __longlong_as_double((long long)(((uint64_t)(e - 7u + 1023u) << 52) | ((uint64_t)m << 49)));
+}
+
+// E4M3 code of RNE(value(c) * gs / gd) for binary32 gs, gd > 0, ties to the
+// even code, saturating at 448.
+__device__ __forceinline__ uint32_t fold_scale_code(uint32_t c, double gs, double gd) {
+  const double num = e4m3_f64(c) * gs;
+  uint32_t lo = 0, hi = 126;                  // largest code lo with value(lo) * gd <= num
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi + 1) >> 1;
+    if (e4m3_f64(mid) * gd <= num) lo = mid;
+    else hi = mid - 1;
+  }
+  if (lo == 126) return 126;
+  const double twice_mid = (e4m3_f64(lo) + e4m3_f64(lo + 1)) * gd;
+  const double twice_num = 2.0 * num;
+  if (twice_num > twice_mid) return lo + 1;
+  if (twice_num < twice_mid) return lo;
+  return (lo & 1u) ? lo + 1 : lo;
+}
+
+__global__ __launch_bounds__(kPackThreads) void harmonize_kernel(uint8_t* __restrict__ packed, uint32_t N,
+                                                                uint32_t kb_valid, uint32_t kc_count,
+                                                                uint32_t scale_offset, SegTable segs,
+                                                                const float* __restrict__ g_seg,
+                                                                float* __restrict__ g_shared) {
+  float gsh = 0.0f;
+  for (int s = 0; s < segs.n_seg; ++s) {
+    const float g = g_seg[s];
+    if (g > 0.0f && (gsh == 0.0f || g < gsh)) gsh = g;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *g_shared = gsh;
+  const uint32_t n_blocks = N * kb_valid;
+  for (uint32_t b = blockIdx.x * kPackThreads + threadIdx.x; b < n_blocks; b += gridDim.x * kPackThreads) {
+    const uint32_t n = b / kb_valid, kb = b - n * kb_valid;
+    const float g = g_seg[segment_of(segs, n)];
+    if (g == 0.0f || g == gsh) continue;     // all-zero segment, or ratio 1
+    uint8_t* sp = packed + scale_offset + packed_scale_offset(n, kb, kc_count);
+    *sp = (uint8_t)fold_scale_code(*sp, (double)gsh, (double)g);
+  }
+}
+
 static SegTable make_segs(const int64_t* seg_offsets, int n_seg) {
   SegTable t{};
   t.n_seg = n_seg;
@@ -156,6 +212,18 @@ hipError_t launch_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
                      wp, (uint32_t)N, (uint32_t)(K / 16), (uint32_t)ldw, kb_pad, n_blocks_pad,
                      (uint32_t)d.kc, segs, (const float*)g_enc_seg,
                      static_cast<uint8_t*>(packed), (uint32_t)d.scale_offset);
+  return hipGetLastError();
+}
+
+hipError_t launch_harmonize_weight(void* packed, int64_t N, int64_t K, const int64_t* seg_offsets,
+                                   int n_seg, const float* g_enc_seg, float* g_shared,
+                                   hipStream_t stream) {
+  SegTable segs = make_segs(seg_offsets, n_seg);
+  PackedDims d = packed_dims(N, K);
+  const uint32_t kb_valid = (uint32_t)(K / 16);
+  hipLaunchKernelGGL(harmonize_kernel, dim3(grid_cap((uint64_t)N * kb_valid, 4096)), dim3(kPackThreads), 0,
+                     stream, static_cast<uint8_t*>(packed), (uint32_t)N, kb_valid, (uint32_t)d.kc,
+                     (uint32_t)d.scale_offset, segs, g_enc_seg, g_shared);
   return hipGetLastError();
 }
 

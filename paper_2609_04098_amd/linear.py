@@ -63,6 +63,15 @@ def unpack_weight(pw: PackedWeight, stream=None):
     return codes, scales
 
 
+def harmonize_weight(pw: PackedWeight, in_place=False, stream=None) -> PackedWeight:
+    """The one-global-scale form of a fused weight group (section 6 repair):
+    a PackedWeight with a single segment whose scale is the shared G."""
+    packed = pw.packed if in_place else pw.packed.clone()
+    g = torch.empty(1, dtype=torch.float32, device=packed.device)
+    _c.nvfp4_harmonize_weight(packed, pw.n, pw.k, pw.seg_offsets, pw.g_seg, g, stream)
+    return PackedWeight(packed, g, pw.n, pw.k, [0, pw.n])
+
+
 def alloc_act(m, k, device) -> QuantizedAct:
     return QuantizedAct(torch.empty((m, k // 2), dtype=torch.uint8, device=device),
                         torch.empty((m, k // 16), dtype=torch.uint8, device=device),

@@ -37,6 +37,7 @@ SIGNATURES = {
     "nvfp4_pack_weight": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _int, _vp, _int, _vp, _sz,
                                  _vp, _sz, _vp]),
     "nvfp4_unpack_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _vp, _vp]),
+    "nvfp4_harmonize_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _int, _vp, _vp, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
                           _c_int64, _int, _vp]),
 }
@@ -73,7 +74,7 @@ def _ptr(t):
 
 def _stream(stream):
     if stream is not None:
-        return ctypes.c_void_p(stream)
+        return ctypes.c_void_p(getattr(stream, "cuda_stream", stream))
     import torch
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -129,6 +130,15 @@ def nvfp4_pack_weight(w, seg_offsets, g_enc_seg, packed, mode=NVFP4_DYNAMIC, wor
 def nvfp4_unpack_weight(packed, N, K, codes, scales, stream=None):
     st = lib().nvfp4_unpack_weight(_ptr(packed), N, K, _ptr(codes), _ptr(scales), _stream(stream))
     _check(st, "nvfp4_unpack_weight")
+
+
+def nvfp4_harmonize_weight(packed, N, K, seg_offsets, g_enc_seg, g_shared, stream=None):
+    """In place: one shared global scale for a fused weight group (written to
+    g_shared, device float [1]), block scales re-rounded accordingly."""
+    offs, n_seg = _offsets(seg_offsets)
+    st = lib().nvfp4_harmonize_weight(_ptr(packed), N, K, offs, n_seg, _ptr(g_enc_seg), _ptr(g_shared),
+                                      _stream(stream))
+    _check(st, "nvfp4_harmonize_weight")
 
 
 def nvfp4_gemm(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y,

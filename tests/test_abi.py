@@ -122,3 +122,20 @@ def test_unpack_rejects_bad_arguments():
     assert f(FAKE, 0, 32, FAKE, FAKE, None) == C.NVFP4_EINVAL
     assert f(FAKE, 8, 24, FAKE, FAKE, None) == C.NVFP4_EINVAL
     assert f(None, 8, 32, FAKE, FAKE, None) == C.NVFP4_EINVAL
+
+
+def test_harmonize_rejects_bad_arguments():
+    f = C.lib().nvfp4_harmonize_weight
+
+    def call(N=32, K=64, offs=(0, 16, 32), n_seg=2, packed=FAKE, g=FAKE, gs=FAKE + 64):
+        return f(packed, N, K, _offs(list(offs)), n_seg, g, gs, None)
+    assert call(K=40) == C.NVFP4_EINVAL
+    assert call(N=0, offs=(0, 0), n_seg=1) == C.NVFP4_EINVAL
+    assert call(offs=(0, 16, 16)) == C.NVFP4_EINVAL
+    assert call(offs=(0, 16, 30)) == C.NVFP4_EINVAL
+    assert call(packed=None) == C.NVFP4_EINVAL
+    assert call(packed=FAKE + 4) == C.NVFP4_EINVAL
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert call(gs=None) == C.NVFP4_EINVAL
+    assert call(gs=FAKE + 4) == C.NVFP4_EINVAL            # g_shared inside g_enc_seg
+    assert call(gs=FAKE + 66) == C.NVFP4_EINVAL           # misaligned

@@ -72,6 +72,9 @@ def test_gemm_tiny_workload():
     (257, 96, 512, [0, 48, 96]),           # tall-skinny path, 48 + 48 segments in one tile
     (64, 40, 48, [0, 40]),                 # tall-skinny path, N not a multiple of 32
     (1, 33, 16, [0, 33]),                  # single row, single block
+    (300, 96, 5184, [0, 48, 96]),          # tall-skinny split-K: 81 chunks over 4 waves
+    (70, 64, 192, [0, 64]),                # tall-skinny split-K: fewer chunks than waves
+    (33, 90, 80, [0, 30, 90]),             # tall-skinny split-K, unaligned K, ragged N
     (513, 520, 1024, [0, 100, 200, 300, 400, 500, 510, 515, 520]),   # 8 segments
 ])
 def test_gemm_ragged_shapes(m, n, k, offs):
