@@ -95,6 +95,18 @@ __device__ __forceinline__ half8 decode8(uint32_t c, half2v s) {
   return half8{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
+// Direct-to-LDS buffer loads: each lane's 16 (or 4) bytes at voffset land at
+// dst + 16 * lane (4 * lane); dst must be the same for the whole wave.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 16, voffset, 0, 0, 0);
+}
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 4, voffset, 0, 0, 0);
+}
+
+// Index of the calling wave in its workgroup, in a scalar register.
+__device__ __forceinline__ uint32_t wave_index() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);     // finite inputs
@@ -425,13 +437,19 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
   store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, m0, n0, r, h);
 }
 
-// Tall-skinny shapes (N <= 96): the output has too few 32 x 32 tiles to give
-// every SIMD two waves, so the KS waves of a workgroup share one FM x FN
-// fragment tile and split its reduction: wave w takes chunks w, w + KS, ...
-// (adjacent chunks of a row are read by adjacent waves at the same time).
-// The partial sums meet in LDS; fragment f is summed (in wave order, so the
-// result is deterministic) and stored by wave f % KS.
-template <int KS, int FM, int FN, int kDepth, bool kF32Out, bool kAlignedK>
+// ----------------------------------------------------------- split-K path
+//
+// Shapes whose output has too few 32 x 32 tiles to give every SIMD two waves
+// (N <= 96: the tall-skinny gate projections; M <= 32: decode-shaped calls,
+// weight-bandwidth-bound): the KS waves of a workgroup share one FM x FN
+// fragment tile and split its reduction, wave w taking chunks w, w + KS, ...
+// Each wave streams its own chunks through a private LDS ring with
+// direct-to-LDS loads (no barrier in the loop; its own memory counter says
+// when a stage has landed), reads the next chunk's raw fragments from LDS
+// while it decodes and multiplies the current one, and the partial sums meet
+// in LDS at the end; fragment f is summed in wave order (deterministic) and
+// stored by wave f % KS.  Requires K % 64 == 0.
+template <int KS, int FM, int FN, int kStages, bool kF32Out>
 __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* __restrict__ a_codes,
                                                              const uint8_t* __restrict__ a_scales,
                                                              const float* __restrict__ a_g,
@@ -439,27 +457,78 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
                                                              const float* __restrict__ w_g,
                                                              void* __restrict__ y, GemmParams p) {
   constexpr int BM = FM * 32, BN = FN * 32;
-  __shared__ floatx16 part[KS][64];
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kFrags = FM + FN;
+  constexpr int kScaleBase = kFrags * 1024;                  // codes 1 KB, then scales 256 B per fragment
+  constexpr int kStageBytes = kFrags * 1280;
+  constexpr int kLoads = 2 * kFrags;                         // DMA loads per chunk and wave
+  constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoads);
+  constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoads);
+  static_assert(kStages >= 2 && (kStages - 1) * kLoads < 64, "memory counter range");
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  // The wave index is uniform: taking it through readfirstlane keeps the
+  // chunk index, buffer descriptors and LDS addresses in scalar registers.
+  const uint32_t lane = threadIdx.x & 63, wave = wave_index();
   const uint32_t r = lane & 31, h = lane >> 5;
   uint32_t tm, tn;
   tile_of<8>(p, tm, tn);
   const uint32_t m0 = tm * BM, n0 = tn * BN;
+  uint8_t* ring = smem + wave * (kStages * kStageBytes);
 
-  uint32_t a_row[FM], b_tile[FN];
+  uint32_t a_off[FM], as_off[FM], b_off[FN], bs_off[FN];
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
-    uint32_t row = m0 + f * 32 + r;
-    a_row[f] = row < p.M ? row : p.M - 1;
+    const uint32_t row = m0 + f * 32 + r;
+    a_off[f] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
+    as_off[f] = row < p.M ? row * (p.K >> 4) : kOOB;
   }
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
-    uint32_t t = (n0 >> 5) + f;
-    b_tile[f] = t < p.w_tiles ? t : p.w_tiles - 1;
+    const uint32_t nt = (n0 >> 5) + f;
+    b_off[f] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+    bs_off[f] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
   }
-  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
-  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
-  const __amdgpu_buffer_rsrc_t rw = rsrc(w_packed, p.w_bytes);
+  const uint8_t* w_scales = w_packed + p.w_scale_offset;
+  const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
+  const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+
+  auto chunk_rsrc = [&](const uint8_t* base, uint32_t bytes, uint32_t step, uint32_t kc) {
+    const uint32_t adv = kc * step;
+    const bool live = kc < p.chunks && adv < bytes;
+    return rsrc(base + (live ? adv : 0u), live ? bytes - adv : 0u);
+  };
+  // DMA of this wave's i-th chunk into stage i % kStages; chunks past the
+  // end of K read zeros.
+  auto issue = [&](uint32_t i) {
+    const uint32_t kc = wave + KS * i;
+    uint8_t* st = ring + (i % kStages) * kStageBytes;
+    const __amdgpu_buffer_rsrc_t ra = chunk_rsrc(a_codes, p.a_code_bytes, 32u, kc);
+    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(a_scales, p.a_scale_bytes, 4u, kc);
+    const __amdgpu_buffer_rsrc_t rb = chunk_rsrc(w_packed, p.w_scale_offset, 1024u, kc);
+    const __amdgpu_buffer_rsrc_t rbs = chunk_rsrc(w_scales, w_scale_bytes, 128u, kc);
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      dma16(ra, st + f * 1024, a_off[f]);
+      dma4(rs, st + kScaleBase + f * 256, as_off[f]);
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      dma16(rb, st + (FM + f) * 1024, b_off[f]);
+      dma4(rbs, st + kScaleBase + (FM + f) * 256, bs_off[f]);
+    }
+  };
+
+  struct Regs {
+    int4v c[kFrags];
+    uint32_t s[kFrags];
+  };
+  auto read_stage = [&](Regs& R, uint32_t i) {
+    const uint8_t* st = ring + (i % kStages) * kStageBytes;
+#pragma unroll
+    for (int f = 0; f < kFrags; ++f) {
+      R.c[f] = *(const int4v*)(st + f * 1024 + lane * 16);
+      R.s[f] = *(const uint32_t*)(st + kScaleBase + f * 256 + lane * 4);
+    }
+  };
 
   floatx16 acc[FM][FN];
 #pragma unroll
@@ -467,47 +536,70 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
 #pragma unroll
     for (int fb = 0; fb < FN; ++fb) acc[fa][fb] = floatx16{};
 
-  // kDepth chunks of this wave in flight: buffer d holds the wave's chunk
-  // i while the loads of its next kDepth - 1 chunks are outstanding.  The
-  // loads are unconditional (a prefetch past the wave's last chunk re-reads
-  // the last chunk of the row) so that the loop body is one basic block and
-  // the memory counter waits only for the chunk about to be used.
-  const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
-  auto kc_of = [&](uint32_t i) -> uint32_t {
-    const uint32_t kc = wave + KS * i;
-    return kc < p.chunks ? kc : p.chunks - 1;
-  };
-  Chunk<FM, FN> buf[kDepth];
+  auto step = [&](uint32_t i, const Regs& cur, Regs& next) {
+    __builtin_amdgcn_s_waitcnt(lds::kWaitLgkm0);       // cur read from its stage
+    __builtin_amdgcn_s_waitcnt(kWaitNext);              // chunk i + 1 landed
+    issue(i + kStages);                                 // refills cur's stage
+    read_stage(next, i + 1);
+    half2v sc[kFrags];
 #pragma unroll
-  for (int d = 0; d < kDepth; ++d) load_chunk<FM, FN, kAlignedK>(buf[d], kc_of(d), p, ra, rs, rw, a_row, b_tile, lane);
-  uint32_t i = 0;
-  for (; i + kDepth <= n_mine; i += kDepth) {
+    for (int f = 0; f < kFrags; ++f) sc[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.s[f] >> (16 * h), 1.0f, false);
+    half8 v[2][kFrags];
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-      mma_chunk<FM, FN>(acc, buf[d]);
-      // Issue the refill here: left to itself the scheduler sinks the loads
-      // to the end of the body and the prefetch distance is lost.
-      __builtin_amdgcn_sched_barrier(0);
-      load_chunk<FM, FN, kAlignedK>(buf[d], kc_of(i + d + kDepth), p, ra, rs, rw, a_row, b_tile, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int f = 0; f < kFrags; ++f) v[0][f] = decode8((uint32_t)cur.c[f][0], __builtin_shufflevector(sc[f], sc[f], 0, 0));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = j & 1;
+      if (j < 3) {
+        const int t = (j + 1) >> 1;
+#pragma unroll
+        for (int f = 0; f < kFrags; ++f)
+          v[u ^ 1][f] = decode8((uint32_t)cur.c[f][j + 1], t ? __builtin_shufflevector(sc[f], sc[f], 1, 1)
+                                                            : __builtin_shufflevector(sc[f], sc[f], 0, 0));
+      }
+#pragma unroll
+      for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+        for (int fb = 0; fb < FN; ++fb)
+          acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(v[u][fa], v[u][FM + fb], acc[fa][fb], 0, 0, 0);
     }
-  }
+    constexpr int kMfma = 4 * FM * FN;
+    constexpr int kValu = (4 * 8 * kFrags + 2 * kFrags + kMfma - 1) / kMfma;
 #pragma unroll
-  for (int d = 0; d < kDepth - 1; ++d)
-    if (i + d < n_mine) mma_chunk<FM, FN>(acc, buf[d]);
+    for (int q = 0; q < kMfma; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);                               // VALU
+      if (q < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                   // VMEM (DMA)
+      if (q < 2 * kFrags) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);               // LDS read
+    }
+  };
 
+#pragma unroll
+  for (int s = 0; s < kStages; ++s) issue(s);
+  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  Regs cur, nxt;
+  read_stage(cur, 0);
+  for (uint32_t i = 0; i < n_mine; ++i) {
+    step(i, cur, nxt);
+    cur = nxt;
+  }
+  // Drain this wave's DMA (chunks past the end) before the ring is reused.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+
+  floatx16* part = reinterpret_cast<floatx16*>(smem);       // [KS][64]
   const float ga = *a_g;
 #pragma unroll
   for (int fa = 0; fa < FM; ++fa) {
 #pragma unroll
     for (int fb = 0; fb < FN; ++fb) {
       const uint32_t owner = (fa * FN + fb) % KS;
-      part[wave][lane] = acc[fa][fb];
+      part[wave * 64 + lane] = acc[fa][fb];
       __syncthreads();
       if (wave == owner) {
-        floatx16 sum = part[0][lane];
+        floatx16 sum = part[lane];
 #pragma unroll
-        for (int w = 1; w < KS; ++w) sum += part[w][lane];
+        for (int w = 1; w < KS; ++w) sum += part[w * 64 + lane];
         const uint32_t col = n0 + fb * 32 + r;
         int s = 0;
 #pragma unroll
@@ -531,23 +623,22 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   }
 }
 
-template <int KS, int FM, int FN, int kDepth>
+template <int KS, int FM, int FN, int kStages>
 static hipError_t launch_splitk(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                                 const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
-                                bool out_f32, bool aligned, hipStream_t stream) {
+                                bool out_f32, hipStream_t stream) {
   constexpr int BM = FM * 32, BN = FN * 32;
+  constexpr int kLds = KS * kStages * (FM + FN) * 1280;
+  static_assert(kLds >= KS * 64 * 64, "the reduction reuses the rings");
   p.tiles_m = (p.M + BM - 1) / BM;
   p.tiles_n = (p.N + BN - 1) / BN;
   const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
-#define NVFP4_G(F32, AL)                                                                               \
-  hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kDepth, F32, AL>), grid, block, 0, stream, a_codes, a_scales, \
-                     a_g, w_packed, w_g, y, p)
-  if (out_f32) {
-    if (aligned) NVFP4_G(true, true); else NVFP4_G(true, false);
-  } else {
-    if (aligned) NVFP4_G(false, true); else NVFP4_G(false, false);
-  }
-#undef NVFP4_G
+  if (out_f32)
+    hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, true>), grid, block, kLds, stream, a_codes,
+                       a_scales, a_g, w_packed, w_g, y, p);
+  else
+    hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, false>), grid, block, kLds, stream, a_codes,
+                       a_scales, a_g, w_packed, w_g, y, p);
   return hipGetLastError();
 }
 
@@ -609,8 +700,10 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     p.seg_off[i] = (uint32_t)seg_offsets[i <= n_seg ? i : n_seg];
   const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   const bool aligned = (K % 64) == 0;
-  if (N <= 96)
-    return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
+  if (aligned && N <= 96)
+    return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+  if (aligned && M <= 32)
+    return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   if (aligned) return launch_lds(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }

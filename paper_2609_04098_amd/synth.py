@@ -73,9 +73,20 @@ CONFIGS = {
     "ab_gates": Config(
         "ab_gates", 4, 32768, 5120, (48, 48), (0.05, 0.05), "residual",
         description="tall-skinny GDN a/b gate projection, 32768x96x5120"),
+    # Decode-shaped calls of the gate/up projection: a batch of 1 or 32
+    # tokens against the full fused weight (weight-bandwidth-bound).
+    "decode_m32": Config(
+        "decode_m32", 5, 32, 5120, (17408, 17408),
+        (0.015 * 1.0, 0.015 * 1.3), "residual",
+        description="decode-shape gate/up projection, 32 tokens, 32x34816x5120"),
+    "decode_m1": Config(
+        "decode_m1", 6, 1, 5120, (17408, 17408),
+        (0.015 * 1.0, 0.015 * 1.3), "residual",
+        description="decode-shape gate/up projection, 1 token, 1x34816x5120"),
 }
 
 CONFIG_ORDER = ["tiny", "gdn_qkv", "mlp_gate_up", "mlp_down", "ab_gates"]
+DECODE_ORDER = ["decode_m32", "decode_m1"]
 
 TENSOR_X = 0
 TENSOR_W = 1

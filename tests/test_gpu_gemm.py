@@ -76,6 +76,9 @@ def test_gemm_tiny_workload():
     (70, 64, 192, [0, 64]),                # tall-skinny split-K: fewer chunks than waves
     (33, 90, 80, [0, 30, 90]),             # tall-skinny split-K, unaligned K, ragged N
     (513, 520, 1024, [0, 100, 200, 300, 400, 500, 510, 515, 520]),   # 8 segments
+    (32, 520, 5120, [0, 260, 520]),        # small-M split-K: 80 chunks over 8 waves, ragged N
+    (1, 300, 1040, [0, 300]),              # small-M, one row, K % 64 != 0
+    (17, 4100, 128, [0, 4000, 4100]),      # small-M, many column tiles, 2 chunks < 8 waves
 ])
 def test_gemm_ragged_shapes(m, n, k, offs):
     rng = np.random.default_rng(m * 7 + n * 3 + k)
@@ -125,11 +128,13 @@ def test_gemm_is_deterministic_and_stays_in_bounds():
 
 
 def _sample_rows(m, rng):
+    if m <= 32:
+        return np.arange(m)
     rows = list(range(8)) + list(range(m - 8, m)) + list(rng.choice(np.arange(8, m - 8), 16, replace=False))
     return np.array(sorted(set(rows)))
 
 
-@pytest.mark.parametrize("name", synth.CONFIG_ORDER)
+@pytest.mark.parametrize("name", synth.CONFIG_ORDER + synth.DECODE_ORDER)
 def test_gemm_full_workloads(name):
     wl = workload(name)
     cfg = wl["cfg"]
