@@ -93,3 +93,18 @@ def bf16_bits_to_f64(bits):
     bits = np.asarray(bits, dtype=np.uint16)
     f32 = (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
     return f32.astype(np.float64)
+
+
+def f64_to_bf16_bits(y):
+    """Round float64 values to bf16 once (round to nearest, ties to even),
+    returning the bit patterns (uint16).  bf16 keeps 8 significant bits down
+    to 2^-126 and is subnormal with spacing 2^-133 below; inputs are finite
+    and inside the bf16 range."""
+    y = np.asarray(y, dtype=np.float64)
+    mag = np.abs(y)
+    m, e = np.frexp(mag)                        # mag = m * 2^e, 0.5 <= m < 1
+    normal = e - 1 >= -126
+    q = np.where(normal, np.rint(np.ldexp(m, 8)), np.rint(np.ldexp(mag, 133)))
+    val = np.where(normal, np.ldexp(q, e - 8), np.ldexp(q, -133))
+    bits = (val.astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    return np.where(np.signbit(y), bits | np.uint16(0x8000), bits).astype(np.uint16)
