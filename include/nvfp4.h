@@ -104,7 +104,35 @@ int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                        uint8_t* codes, uint8_t* scales, float* g_enc, int mode,
                        void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
+/*
+ * RMSNorm fused with activation quantization under a calibrated (static)
+ * global scale: one pass over the activations (the paper serves its W4A4
+ * model with activation scales calibrated offline, section 3 "Checkpoints";
+ * NVFP4 itself: section 2).
+ *
+ *   y = RNE_bf16((x * r) * gamma),  r = 1 / sqrt(sum_k x^2 / K + eps),
+ *   evaluated in binary32 per row (the sum of squares in a fixed order, r with
+ *   correctly rounded division and square root);
+ *   codes, scales = the NVFP4 quantization of y under G = *g_enc, exactly as
+ *   nvfp4_quantize_act in NVFP4_STATIC mode would write them for y.
+ *
+ *   x       bf16 [M x K], row stride ldx elements (ldx >= K, ldx % 8 == 0).
+ *   gamma   bf16 [K] (device).
+ *   eps     >= 0, finite.
+ *   codes, scales   out, as for nvfp4_quantize_act (contiguous rows).
+ *   g_enc   device float: the calibrated G (read only).
+ *   y       optional out (may be NULL): the normalized bf16 [M x K], row
+ *           stride ldy elements.
+ * Requirements: M >= 0, K >= 16, K % 16 == 0, M * ldx < 2^31; pointers
+ * 16-byte aligned (g_enc 4-byte).  M == 0 enqueues nothing.
+ * Errors: NVFP4_EINVAL, NVFP4_EUNSUPPORTED, NVFP4_EHIP.
+ */
+int nvfp4_rmsnorm_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
+                               const void* gamma, float eps, uint8_t* codes,
+                               uint8_t* scales, const float* g_enc, void* y,
+                               int64_t ldy, void* stream);
+
+/* Bytes of the packed weight buffer for an N x K weight:/* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
  * tile layout of the codes and block scales, N padded to 32 and K to 64. */
 size_t nvfp4_packed_weight_bytes(int64_t N, int64_t K);
 

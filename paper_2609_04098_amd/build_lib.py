@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnvfp4.so")
 
-SOURCES = ["api.cpp", "act_quant.hip", "weight_pack.hip", "gemm.hip"]
+SOURCES = ["api.cpp", "act_quant.hip", "norm_quant.hip", "weight_pack.hip", "gemm.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

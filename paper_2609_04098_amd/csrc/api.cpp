@@ -5,6 +5,7 @@
 // kept per host thread.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <math.h>
 #include <string.h>
 
 #include <mutex>
@@ -104,6 +105,26 @@ int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t
   hipError_t e = nvfp4::launch_act_quant(x, M, K, ldx, codes, scales, g_enc, dynamic,
                                          static_cast<float*>(workspace),
                                          static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
+int nvfp4_rmsnorm_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx, const void* gamma,
+                               float eps, uint8_t* codes, uint8_t* scales, const float* g_enc, void* y,
+                               int64_t ldy, void* stream) {
+  if (M < 0 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
+  if (!(eps >= 0.0f) || !isfinite(eps)) return NVFP4_EINVAL;
+  if (g_enc == nullptr || (reinterpret_cast<uintptr_t>(g_enc) & 3u)) return NVFP4_EINVAL;
+  if (gamma == nullptr || !aligned16(gamma)) return NVFP4_EINVAL;
+  if (M > 0) {
+    if (ldx < K || ldx % 8 != 0 || M * ldx >= kI32Lim || M * K >= kI32Lim) return NVFP4_EINVAL;
+    if (x == nullptr || codes == nullptr || scales == nullptr) return NVFP4_EINVAL;
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(scales)) return NVFP4_EINVAL;
+    if (y != nullptr && (ldy < K || ldy % 8 != 0 || M * ldy >= kI32Lim || !aligned16(y))) return NVFP4_EINVAL;
+  }
+  int st = check_device();
+  if (st != NVFP4_OK) return st;
+  hipError_t e = nvfp4::launch_rmsnorm_quant(x, M, K, ldx, gamma, eps, g_enc, codes, scales, y, ldy,
+                                             static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 

@@ -21,6 +21,10 @@ hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, ui
                             uint8_t* scales, float* g_enc, bool dynamic, float* partial,
                             hipStream_t stream);
 
+hipError_t launch_rmsnorm_quant(const void* x, int64_t M, int64_t K, int64_t ldx, const void* gamma,
+                                float eps, const float* g_enc, uint8_t* codes, uint8_t* scales, void* y,
+                                int64_t ldy, hipStream_t stream);
+
 hipError_t launch_pack_weight(const void* w, int64_t N, int64_t K, int64_t ldw,
                               const int64_t* seg_offsets, int n_seg, float* g_enc_seg,
                               bool dynamic, void* packed, float* partial, hipStream_t stream);

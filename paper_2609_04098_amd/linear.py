@@ -96,6 +96,19 @@ def quantize_act(x, g=None, out: QuantizedAct = None, workspace=None, stream=Non
     return aq
 
 
+def rmsnorm_quantize_act(x, gamma, eps, g, out: QuantizedAct = None, y=None, stream=None) -> QuantizedAct:
+    """RMSNorm of a bf16 [M, K] activation fused with its quantization under
+    the calibrated global scale ``g`` (a float or a device float32 [1])."""
+    m, k = x.shape
+    aq = alloc_act(m, k, x.device) if out is None else out
+    if torch.is_tensor(g):
+        aq.g.copy_(g.reshape(1))
+    else:
+        aq.g.copy_(torch.as_tensor([float(g)], dtype=torch.float32))
+    _c.nvfp4_rmsnorm_quantize_act(x, gamma, eps, aq.codes, aq.scales, aq.g, y, stream)
+    return aq
+
+
 def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None, stream=None):
     if aq.k != pw.k:
         raise ValueError("K mismatch between activation and weight")

@@ -32,6 +32,8 @@ SIGNATURES = {
     "nvfp4_last_hip_error": (_int, []),
     "nvfp4_quantize_act_workspace_bytes": (_sz, [_c_int64, _c_int64]),
     "nvfp4_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _vp, _vp, _int, _vp, _sz, _vp]),
+    "nvfp4_rmsnorm_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, ctypes.c_float, _vp, _vp,
+                                           _vp, _vp, _c_int64, _vp]),
     "nvfp4_packed_weight_bytes": (_sz, [_c_int64, _c_int64]),
     "nvfp4_pack_weight_workspace_bytes": (_sz, [_c_int64, _c_int64, _int]),
     "nvfp4_pack_weight": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _int, _vp, _int, _vp, _sz,
@@ -113,6 +115,17 @@ def nvfp4_quantize_act(x, codes, scales, g_enc, mode=NVFP4_DYNAMIC, workspace=No
     st = lib().nvfp4_quantize_act(_ptr(x), M, K, ldx, _ptr(codes), _ptr(scales), _ptr(g_enc), mode,
                                   _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "nvfp4_quantize_act")
+
+
+def nvfp4_rmsnorm_quantize_act(x, gamma, eps, codes, scales, g_enc, y=None, stream=None):
+    """x bf16 [M, K] (row stride x.stride(0)); gamma bf16 [K]; g_enc float32
+    [1] (the calibrated G); codes uint8 [M, K/2]; scales uint8 [M, K/16];
+    y optional bf16 [M, K] output of the normalization."""
+    M, K = x.shape
+    ldy = 0 if y is None else y.stride(0)
+    st = lib().nvfp4_rmsnorm_quantize_act(_ptr(x), M, K, x.stride(0), _ptr(gamma), float(eps), _ptr(codes),
+                                          _ptr(scales), _ptr(g_enc), _ptr(y), ldy, _stream(stream))
+    _check(st, "nvfp4_rmsnorm_quantize_act")
 
 
 def nvfp4_pack_weight(w, seg_offsets, g_enc_seg, packed, mode=NVFP4_DYNAMIC, workspace=None,

@@ -139,3 +139,34 @@ def test_harmonize_rejects_bad_arguments():
     assert call(gs=None) == C.NVFP4_EINVAL
     assert call(gs=FAKE + 4) == C.NVFP4_EINVAL            # g_shared inside g_enc_seg
     assert call(gs=FAKE + 66) == C.NVFP4_EINVAL           # misaligned
+
+
+def test_library_has_no_unresolved_own_symbols():
+    """Every kernel the launchers reference is defined in the library (a
+    kernel template whose host stub is not emitted shows up as an undefined
+    symbol only when the library is loaded with lazy binding)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", C.LIB_PATH], capture_output=True, text=True)
+    assert out.returncode == 0
+    own = [l for l in out.stdout.splitlines() if "nvfp4" in l]
+    assert not own, own
+
+
+def test_rmsnorm_quantize_rejects_bad_arguments():
+    f = C.lib().nvfp4_rmsnorm_quantize_act
+
+    def call(M=8, K=64, ldx=64, gamma=FAKE, eps=1e-6, codes=FAKE, g=FAKE, y=None, ldy=0, x=FAKE):
+        return f(x, M, K, ldx, gamma, eps, codes, FAKE, g, y, ldy, None)
+    assert call(K=40) == C.NVFP4_EINVAL
+    assert call(K=0) == C.NVFP4_EINVAL
+    assert call(ldx=32) == C.NVFP4_EINVAL
+    assert call(eps=-1.0) == C.NVFP4_EINVAL
+    assert call(eps=float("inf")) == C.NVFP4_EINVAL
+    assert call(eps=float("nan")) == C.NVFP4_EINVAL
+    assert call(gamma=None) == C.NVFP4_EINVAL
+    assert call(gamma=FAKE + 8) == C.NVFP4_EINVAL
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert call(codes=None) == C.NVFP4_EINVAL
+    assert call(y=FAKE, ldy=32) == C.NVFP4_EINVAL
+    assert call(y=FAKE + 8, ldy=64) == C.NVFP4_EINVAL
+    assert call(x=FAKE + 2) == C.NVFP4_EINVAL
