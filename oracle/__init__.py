@@ -20,6 +20,7 @@ vs. fused-GEMM scaling"):
   used by the tolerance.
 * ``harmonize`` the repair of section 6 for a fused weight group: one shared
   global scale with the ratio folded into re-rounded E4M3 block scales.
+* ``gates``    the GDN gate transform (Eq. 1) of the fused a/b projection.
 * ``norm``     RMSNorm in front of the quantizer (for the one-pass
   normalize-and-quantize path with a calibrated activation scale).
 * ``stats``    block statistics of Table 2 (max/RMS, kurtosis, one-hot blocks,
@@ -30,4 +31,4 @@ every product that is compared, see ``quant``), so codes and scales are a
 function of the inputs alone, independent of any operation order.
 """
 
-from . import formats, quant, gemm, harmonize, norm, stats  # noqa: F401
+from . import formats, gates, quant, gemm, harmonize, norm, stats  # noqa: F401
