@@ -215,6 +215,25 @@ def main():
     norm_avg = time_one_pass(
         lambda: C.nvfp4_rmsnorm_quantize_act(x, gamma, 1e-6, aq.codes, aq.scales, aq.g, None, stream))
     del flush
+
+    gates = None
+    if cfg.n <= 96 and cfg.n % 2 == 0 and cfg.k % 64 == 0 and len(cfg.segments) == 2:
+        # The tall-skinny b|a gate projection with the GDN gate transform
+        # (Eq. 1) in its epilogue, timed like the plain GEMM.
+        h = cfg.n // 2
+        rng = np.random.default_rng(99)
+        a_log = torch.from_numpy(np.log(rng.uniform(1.0, 16.0, h)).astype(np.float32)).to(dev)
+        dt_bias = torch.from_numpy(rng.uniform(-4.0, 2.0, h).astype(np.float32)).to(dev)
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            L.quantize_act(x, out=aq, workspace=ws)
+            gev[i][0].record(stream)
+            L.gemm_gdn_gates(aq, pw, a_log, dt_bias, out=y)
+            gev[i][1].record(stream)
+        torch.cuda.synchronize()
+        gates_avg = float(np.mean([a.elapsed_time(b) for a, b in gev]))
+        gates = {"avg_ms": round(gates_avg, 4), "plain_gemm_avg_ms": round(gemm_avg, 4),
+                 "note": "GEMM with the GDN gate transform (beta | alpha) in the epilogue"}
     aq_static_gbs = aq_bytes / (aq_static_avg * 1e-3) / 1e9
     norm_gbs = aq_bytes / (norm_avg * 1e-3) / 1e9
     log("step %.3f ms (events %.3f), act-quant %.3f ms, GEMM %.3f ms" % (
@@ -269,6 +288,7 @@ def main():
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(norm_gbs / HBM_PEAK_GBS, 4),
             "note": "RMSNorm fused with the static-scale quantizer, one pass, X from HBM (median); not part of value",
         },
+        "gdn_gates": gates,
         "frac_of_mxfp4_peak": round(value / MXFP4_PEAK_TFLOPS, 4),
         "prepack_ms": round(prepack_ms, 3),
         "gemm_source_sha256_16": gemm_source_hash(),

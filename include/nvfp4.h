@@ -220,6 +220,30 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg,
                void* y, int64_t ldy, int y_dtype, void* stream);
 
+/*
+ * The fused GDN gate projection with the gate transform in its epilogue
+ * (paper, Eq. 1; the b and a projections are served as one fused GEMM,
+ * section 6).  The weight is the fused [b; a] projection packed by
+ * nvfp4_pack_weight with N = 2H and segments [0, H, 2H] (b rows first).
+ * For token m and head h, with v = the segment-scaled GEMM output:
+ *   y[m, h]     = beta  = 1 / (1 + exp(-v_b))
+ *   y[m, H + h] = alpha = exp(-exp(A_log[h]) * softplus(v_a + dt_bias[h]))
+ * evaluated in binary32 (softplus(x) = log1p(exp(x)), and x for x > 20).
+ *
+ *   a_codes, a_scales, a_g_enc   as for nvfp4_gemm.
+ *   w_packed     the packed [b; a] weight (N = 2H rows).
+ *   w_g_enc_seg  device float [2]: G_W of the b and a segments.
+ *   a_log, dt_bias   device float [H].
+ *   y            out, [M x 2H] (beta | alpha), row stride ldy >= 2H, bf16 or
+ *                float per y_dtype.
+ * Requirements: as for nvfp4_gemm; K % 64 == 0 (NVFP4_EUNSUPPORTED otherwise).
+ */
+int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales,
+                         const float* a_g_enc, int64_t M, int64_t K,
+                         const void* w_packed, int64_t H, const float* w_g_enc_seg,
+                         const float* a_log, const float* dt_bias,
+                         void* y, int64_t ldy, int y_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

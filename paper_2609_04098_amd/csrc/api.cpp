@@ -66,7 +66,7 @@ const char* nvfp4_status_string(int status) {
   switch (status) {
     case NVFP4_OK: return "NVFP4_OK";
     case NVFP4_EINVAL: return "NVFP4_EINVAL: invalid argument";
-    case NVFP4_EUNSUPPORTED: return "NVFP4_EUNSUPPORTED: device is not gfx950";
+    case NVFP4_EUNSUPPORTED: return "NVFP4_EUNSUPPORTED: device is not gfx950, or the shape is not supported";
     case NVFP4_EWORKSPACE: return "NVFP4_EWORKSPACE: workspace or buffer too small";
     case NVFP4_EHIP: return "NVFP4_EHIP: HIP runtime error";
     default: return "NVFP4: unknown status";
@@ -221,6 +221,38 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g
   hipError_t e = nvfp4::launch_gemm(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg,
                                     w_g_enc_seg, y, ldy, y_dtype == NVFP4_OUT_F32,
                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
+int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
+                         int64_t K, const void* w_packed, int64_t H, const float* w_g_enc_seg,
+                         const float* a_log, const float* dt_bias, void* y, int64_t ldy, int y_dtype,
+                         void* stream) {
+  if (y_dtype != NVFP4_OUT_BF16 && y_dtype != NVFP4_OUT_F32) return NVFP4_EINVAL;
+  if (M < 0 || H < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
+  const int64_t N = 2 * H;
+  if (ldy < N) return NVFP4_EINVAL;
+  if (M * K >= kI32Lim || N * K >= kI32Lim || M * ldy >= kI32Lim) return NVFP4_EINVAL;
+  if (nvfp4::packed_dims(N, K).bytes >= kI32Lim) return NVFP4_EINVAL;
+  if (a_g_enc == nullptr || w_g_enc_seg == nullptr || w_packed == nullptr || a_log == nullptr ||
+      dt_bias == nullptr)
+    return NVFP4_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(a_g_enc) & 3u) || (reinterpret_cast<uintptr_t>(w_g_enc_seg) & 3u) ||
+      (reinterpret_cast<uintptr_t>(a_log) & 3u) || (reinterpret_cast<uintptr_t>(dt_bias) & 3u))
+    return NVFP4_EINVAL;
+  if (!aligned16(w_packed)) return NVFP4_EINVAL;
+  if (M > 0) {
+    if (a_codes == nullptr || a_scales == nullptr || y == nullptr) return NVFP4_EINVAL;
+    if (!aligned16(a_codes) || !aligned16(a_scales)) return NVFP4_EINVAL;
+    const uintptr_t elem = y_dtype == NVFP4_OUT_F32 ? 4u : 2u;
+    if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
+  }
+  if (K % 64 != 0) return NVFP4_EUNSUPPORTED;
+  int st = check_device();
+  if (st != NVFP4_OK) return st;
+  hipError_t e = nvfp4::launch_gemm_gdn_gates(a_codes, a_scales, a_g_enc, M, K, w_packed, H, w_g_enc_seg, a_log,
+                                              dt_bias, y, ldy, y_dtype == NVFP4_OUT_F32,
+                                              static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 

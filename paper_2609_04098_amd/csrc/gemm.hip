@@ -71,7 +71,23 @@ struct GemmParams {
   uint32_t tiles_m, tiles_n;
   int n_seg;
   uint32_t seg_off[NVFP4_SEG_TABLE];
+  // GDN gate epilogue (split-K kernel only): H b-columns, then H a-columns.
+  const float* gate_a_log;
+  const float* gate_dt_bias;
+  uint32_t gate_h;
 };
+
+// The GDN gates of paper Eq. 1 from the scaled fused b|a projection v of
+// column col: beta = sigmoid(b) for the first H columns; for the a-columns
+// alpha = exp(-exp(A_log[h]) * softplus(a + dt_bias[h])), softplus taken as
+// its argument above 20 (where log(1 + e^x) equals it to 2e-9 relative).
+__device__ __forceinline__ float gdn_gate(float v, uint32_t col, const GemmParams& p) {
+  if (col < p.gate_h) return 1.0f / (1.0f + expf(-v));
+  const uint32_t h = col - p.gate_h;
+  const float x = v + p.gate_dt_bias[h];
+  const float sp = x > 20.0f ? x : log1pf(expf(x));
+  return expf(-expf(p.gate_a_log[h]) * sp);
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -449,7 +465,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
 // while it decodes and multiplies the current one, and the partial sums meet
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
-template <int KS, int FM, int FN, int kStages, bool kF32Out>
+template <int KS, int FM, int FN, int kStages, bool kF32Out, bool kGate>
 __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* __restrict__ a_codes,
                                                              const uint8_t* __restrict__ a_scales,
                                                              const float* __restrict__ a_g,
@@ -610,7 +626,8 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
         for (int i = 0; i < 16; ++i) {
           const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
           if (row < p.M && col < p.N) {
-            const float v = sum[i] * alpha;
+            float v = sum[i] * alpha;
+            if (kGate) v = gdn_gate(v, col, p);
             if (kF32Out)
               static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
             else
@@ -626,19 +643,22 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
 template <int KS, int FM, int FN, int kStages>
 static hipError_t launch_splitk(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                                 const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
-                                bool out_f32, hipStream_t stream) {
+                                bool out_f32, bool gate, hipStream_t stream) {
   constexpr int BM = FM * 32, BN = FN * 32;
   constexpr int kLds = KS * kStages * (FM + FN) * 1280;
   static_assert(kLds >= KS * 64 * 64, "the reduction reuses the rings");
   p.tiles_m = (p.M + BM - 1) / BM;
   p.tiles_n = (p.N + BN - 1) / BN;
   const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
-  if (out_f32)
-    hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, true>), grid, block, kLds, stream, a_codes,
-                       a_scales, a_g, w_packed, w_g, y, p);
-  else
-    hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, false>), grid, block, kLds, stream, a_codes,
-                       a_scales, a_g, w_packed, w_g, y, p);
+#define NVFP4_SK(F32, GATE)                                                                           \
+  hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, F32, GATE>), grid, block, kLds, stream, \
+                     a_codes, a_scales, a_g, w_packed, w_g, y, p)
+  if (gate) {
+    if (out_f32) NVFP4_SK(true, true); else NVFP4_SK(false, true);
+  } else {
+    if (out_f32) NVFP4_SK(true, false); else NVFP4_SK(false, false);
+  }
+#undef NVFP4_SK
   return hipGetLastError();
 }
 
@@ -677,11 +697,8 @@ static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, co
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
-                       int64_t M, int64_t K, const void* w_packed, int64_t N,
-                       const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
-                       int64_t ldy, bool out_f32, hipStream_t stream) {
-  if (M == 0) return hipSuccess;
+static GemmParams gemm_params(int64_t M, int64_t K, int64_t N, const int64_t* seg_offsets, int n_seg,
+                              int64_t ldy) {
   PackedDims d = packed_dims(N, K);
   GemmParams p{};
   p.M = (uint32_t)M;
@@ -698,14 +715,37 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   p.n_seg = n_seg;
   for (int i = 0; i < NVFP4_SEG_TABLE; ++i)
     p.seg_off[i] = (uint32_t)seg_offsets[i <= n_seg ? i : n_seg];
+  return p;
+}
+
+hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                       int64_t M, int64_t K, const void* w_packed, int64_t N,
+                       const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
+                       int64_t ldy, bool out_f32, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
   const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   const bool aligned = (K % 64) == 0;
   if (aligned && N <= 96)
-    return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+    return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
   if (aligned && M <= 32)
-    return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+    return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
   if (aligned) return launch_lds(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
+}
+
+hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
+                                 int64_t M, int64_t K, const void* w_packed, int64_t H, const float* w_g,
+                                 const float* a_log, const float* dt_bias, void* y, int64_t ldy,
+                                 bool out_f32, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const int64_t offs[3] = {0, H, 2 * H};
+  GemmParams p = gemm_params(M, K, 2 * H, offs, 2, ldy);
+  p.gate_a_log = a_log;
+  p.gate_dt_bias = dt_bias;
+  p.gate_h = (uint32_t)H;
+  return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, static_cast<const uint8_t*>(w_packed), w_g, y, p,
+                                   out_f32, true, stream);
 }
 
 }  // namespace nvfp4

@@ -119,6 +119,19 @@ def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None,
     return y
 
 
+def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype=torch.bfloat16, out=None,
+                   stream=None):
+    """(beta | alpha) [M, 2H] from the fused [b; a] gate projection (Eq. 1)."""
+    h = pw.n // 2
+    if pw.seg_offsets != [0, h, 2 * h]:
+        raise ValueError("the gate weight must be packed as two segments [b; a] of equal width")
+    y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=aq.codes.device)
+    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    _c.nvfp4_gemm_gdn_gates(aq.codes, aq.scales, aq.g, pw.packed, h, pw.g_seg, a_log, dt_bias, y, kind, stream,
+                            M=aq.m, K=aq.k)
+    return y
+
+
 def linear(x, pw: PackedWeight, out_dtype=torch.bfloat16):
     """y = x W^T through NVFP4 W4A4: dynamic act-quant, then the GEMM."""
     return gemm(quantize_act(x), pw, out_dtype)

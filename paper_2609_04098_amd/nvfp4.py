@@ -40,6 +40,8 @@ SIGNATURES = {
                                  _vp, _sz, _vp]),
     "nvfp4_unpack_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _vp, _vp]),
     "nvfp4_harmonize_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _int, _vp, _vp, _vp]),
+    "nvfp4_gemm_gdn_gates": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _vp, _vp, _vp,
+                                    _c_int64, _int, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
                           _c_int64, _int, _vp]),
 }
@@ -165,3 +167,14 @@ def nvfp4_gemm(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg
                           offs, n_seg, _ptr(w_g_enc_seg), _ptr(y), y.stride(0), y_dtype,
                           _stream(stream))
     _check(st, "nvfp4_gemm")
+
+
+def nvfp4_gemm_gdn_gates(a_codes, a_scales, a_g_enc, w_packed, H, w_g_enc_seg, a_log, dt_bias, y,
+                         y_dtype=NVFP4_OUT_BF16, stream=None, M=None, K=None):
+    """y [M, 2H] = (beta | alpha) of the fused b|a gate projection."""
+    M = a_codes.shape[0] if M is None else M
+    K = 2 * a_codes.shape[1] if K is None else K
+    st = lib().nvfp4_gemm_gdn_gates(_ptr(a_codes), _ptr(a_scales), _ptr(a_g_enc), M, K, _ptr(w_packed), H,
+                                    _ptr(w_g_enc_seg), _ptr(a_log), _ptr(dt_bias), _ptr(y), y.stride(0), y_dtype,
+                                    _stream(stream))
+    _check(st, "nvfp4_gemm_gdn_gates")

@@ -170,3 +170,17 @@ def test_rmsnorm_quantize_rejects_bad_arguments():
     assert call(y=FAKE, ldy=32) == C.NVFP4_EINVAL
     assert call(y=FAKE + 8, ldy=64) == C.NVFP4_EINVAL
     assert call(x=FAKE + 2) == C.NVFP4_EINVAL
+
+
+def test_gdn_gates_rejects_bad_arguments():
+    f = C.lib().nvfp4_gemm_gdn_gates
+
+    def call(M=16, K=128, H=48, ldy=96, dtype=0, alog=FAKE, dt=FAKE, y=FAKE, a=FAKE):
+        return f(a, FAKE, FAKE, M, K, FAKE, H, FAKE, alog, dt, y, ldy, dtype, None)
+    assert call(H=0) == C.NVFP4_EINVAL
+    assert call(ldy=95) == C.NVFP4_EINVAL
+    assert call(alog=None) == C.NVFP4_EINVAL
+    assert call(dt=FAKE + 2) == C.NVFP4_EINVAL
+    assert call(y=None) == C.NVFP4_EINVAL
+    assert call(dtype=3) == C.NVFP4_EINVAL
+    assert call(K=80) == C.NVFP4_EUNSUPPORTED       # the gate epilogue needs K % 64 == 0
