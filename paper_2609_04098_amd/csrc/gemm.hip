@@ -211,7 +211,7 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
                                                                    void* __restrict__ y, GemmParams p) {
   using namespace lds;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t lane = threadIdx.x & 63, wave = wave_index();
   const uint32_t r = lane & 31, h = lane >> 5;
   uint32_t tm, tn;
   tile_of<kGroupM>(p, tm, tn);
@@ -257,19 +257,21 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
 
   struct Regs {
     int4v ca[FM], cb[FN];
-    uint32_t sa[FM], sb[FN];
+    uint32_t sa[FM], sb[FN];   // low 16 bits: the lane's two block scales
   };
+  // Lanes r and 32 + r share their scale dword; each reads its own half
+  // (blocks 2h, 2h + 1 of the chunk).
   auto read_stage = [&](Regs& R, uint32_t kc) {
     const uint8_t* st = smem + (kc % kStages) * kStageBytes;
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
-      R.sa[f] = *(const uint32_t*)(st + kSA + (wm * FM + f) * 256 + lane * 4);
+      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * 256 + lane * 4 + h * 2);
     }
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
-      R.sb[f] = *(const uint32_t*)(st + kSB + (wn * FN + f) * 256 + lane * 4);
+      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * 256 + lane * 4 + h * 2);
     }
   };
 
@@ -290,9 +292,9 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
     // Both block scales of the lane (blocks 2h, 2h+1 of the chunk) as FP16.
     half2v sA[FM], sB[FN];
 #pragma unroll
-    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sa[f] >> (16 * h), 1.0f, false);
+    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sa[f], 1.0f, false);
 #pragma unroll
-    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sb[f] >> (16 * h), 1.0f, false);
+    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sb[f], 1.0f, false);
     half8 av[2][FM], bv[2][FN];
 #pragma unroll
     for (int f = 0; f < FM; ++f) av[0][f] = decode8((uint32_t)cur.ca[f][0], __builtin_shufflevector(sA[f], sA[f], 0, 0));
