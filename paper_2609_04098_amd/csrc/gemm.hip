@@ -180,56 +180,73 @@ __device__ __forceinline__ void store_tile(const floatx16 (&acc)[FM][FN], const 
 // ------------------------------------------------------------------ LDS path
 
 namespace lds {
-constexpr int WM = 2, WN = 2, FM = 4, FN = 2;
-constexpr int kThreads = WM * WN * 64;
-constexpr int BM = WM * FM * 32, BN = WN * FN * 32;        // 256 x 128
-constexpr int NFA = WM * FM, NFB = WN * FN;                 // 8 A and 4 B fragments per workgroup
-// One stage of the ring: raw codes (1 KB per fragment) and scales (256 B per
-// fragment: one dword per lane) of one 64-deep chunk.
-constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 256;
-constexpr int kStageBytes = kSB + NFB * 256;               // 15 KB
-constexpr int kStages = 4;
-constexpr int kLdsBytes = kStages * kStageBytes;           // 60 KB: two workgroups per CU
-constexpr int kLoadsPerWave = 6;                           // 2 A code + 2 A scale + 1 B code + 1 B scale
-constexpr int kGroupM = 4;
-constexpr int kValuPerMfma = 5;                            // schedule: VALU slots after each MFMA
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits [3:0] and [15:14],
 // expcnt [6:4], lgkmcnt [11:8]; all-ones means "do not wait").
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int kWaitFirst = vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
-constexpr int kWaitNext = vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c+1 landed
 constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt(0)
-static_assert(NFA == 2 * WM * WN && NFB == WM * WN, "load assignment: 2 A and 1 B fragment per wave");
 }  // namespace lds
 
-template <bool kF32Out>
-__global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
+// Workgroup shape of the LDS kernel: 2 x WN waves, each owning a 128 x 64
+// block of the output (4 x 2 accumulator fragments, 128 registers), so every
+// SIMD runs two waves.  WN = 2 (two 256 x 128 workgroups per CU) is the one
+// launched: WN = 4 (one 256 x 256 workgroup per CU, a third less operand
+// traffic per MFMA) measured 2-15% slower, as did rings of 3 or 5 stages.
+template <int WN_>
+struct LdsCfg {
+  static constexpr int WM = 2, WN = WN_, FM = 4, FN = 2;
+  static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
+  static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
+  static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
+  // One stage of the ring: raw codes (1 KB per fragment) and scales (256 B
+  // per fragment: one dword per lane) of one 64-deep chunk.
+  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 256;
+  static constexpr int kStageBytes = kSB + NFB * 256;
+  static constexpr int kStages = 4;
+  static constexpr int kLdsBytes = kStages * kStageBytes;
+  // Each wave moves the same number of A and B fragments (codes + scales).
+  static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
+  static constexpr int kLoadsPerWave = 2 * (kAPerWave + kBPerWave);
+  static constexpr int kGroupM = 4;
+  static constexpr int kValuPerMfma = 5;                      // schedule: VALU slots after each MFMA
+  static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
+  static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c+1 landed
+  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
+};
+
+template <int WN_, bool kF32Out>
+__global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
                                                                    const uint8_t* __restrict__ a_scales,
                                                                    const float* __restrict__ a_g,
                                                                    const uint8_t* __restrict__ w_packed,
                                                                    const float* __restrict__ w_g,
                                                                    void* __restrict__ y, GemmParams p) {
-  using namespace lds;
+  using C = LdsCfg<WN_>;
+  constexpr int WN = C::WN, FM = C::FM, FN = C::FN, BM = C::BM, BN = C::BN;
+  constexpr int kA = C::kA, kB = C::kB, kSA = C::kSA, kSB = C::kSB, kStages = C::kStages;
+  constexpr int kStageBytes = C::kStageBytes, kAPerWave = C::kAPerWave, kBPerWave = C::kBPerWave;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const uint32_t lane = threadIdx.x & 63, wave = wave_index();
   const uint32_t r = lane & 31, h = lane >> 5;
   uint32_t tm, tn;
-  tile_of<kGroupM>(p, tm, tn);
+  tile_of<C::kGroupM>(p, tm, tn);
   const uint32_t wm = wave / WN, wn = wave % WN;
 
   // Per-lane offsets are fixed; the chunk advances the descriptors' base
   // (and shrinks their size) in scalar registers.  Rows >= M and tiles past
   // the packed weight get offsets beyond every descriptor: zeros.
-  uint32_t a_off[2], as_off[2];
+  uint32_t a_off[kAPerWave], as_off[kAPerWave], b_off[kBPerWave], bs_off[kBPerWave];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const uint32_t row = tm * BM + (2 * wave + i) * 32 + r;
+  for (int i = 0; i < kAPerWave; ++i) {
+    const uint32_t row = tm * BM + (kAPerWave * wave + i) * 32 + r;
     a_off[i] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
     as_off[i] = row < p.M ? row * (p.K >> 4) : kOOB;
   }
-  const uint32_t nt = tn * (BN / 32) + wave;
-  const uint32_t b_off = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
-  const uint32_t bs_off = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+#pragma unroll
+  for (int i = 0; i < kBPerWave; ++i) {
+    const uint32_t nt = tn * (BN / 32) + kBPerWave * wave + i;
+    b_off[i] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+    bs_off[i] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+  }
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
 
@@ -246,13 +263,17 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
     const __amdgpu_buffer_rsrc_t rb = chunk_rsrc(w_packed, p.w_scale_offset, 1024u, kc);
     const __amdgpu_buffer_rsrc_t rbs = chunk_rsrc(w_scales, w_scale_bytes, 128u, kc);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint32_t f = 2 * wave + i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (NVFP4_LDS void*)(st + kA + f * 1024), 16, a_off[i], 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)(st + kSA + f * 256), 4, as_off[i], 0, 0, 0);
+    for (int i = 0; i < kAPerWave; ++i) {
+      const uint32_t f = kAPerWave * wave + i;
+      dma16(ra, st + kA + f * 1024, a_off[i]);
+      dma4(rs, st + kSA + f * 256, as_off[i]);
     }
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (NVFP4_LDS void*)(st + kB + wave * 1024), 16, b_off, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs, (NVFP4_LDS void*)(st + kSB + wave * 256), 4, bs_off, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kBPerWave; ++i) {
+      const uint32_t f = kBPerWave * wave + i;
+      dma16(rb, st + kB + f * 1024, b_off[i]);
+      dma4(rbs, st + kSB + f * 256, bs_off[i]);
+    }
   };
 
   struct Regs {
@@ -284,8 +305,8 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
   // One chunk: wait, barrier, DMA of chunk c + kStages, LDS reads of chunk
   // c+1 into `next`, decode + MFMA of `cur`.
   auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_s_waitcnt(kWaitNext);
+    __builtin_amdgcn_s_waitcnt(lds::kWaitLgkm0);
+    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
     __builtin_amdgcn_s_barrier();
     issue(c + kStages);
     read_stage(next, c + 1);
@@ -321,15 +342,16 @@ __global__ __launch_bounds__(lds::kThreads, 2) void gemm_lds_kernel(const uint8_
 #pragma unroll
     for (int i = 0; i < 4 * FM * FN; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);            // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
       if (i % 2 == 1 && i < 24) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
-      if (i % 4 == 0 && i < 24) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM (DMA)
+      if (i % 4 == 0 && i < 4 * C::kLoadsPerWave)
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
     }
   };
 
 #pragma unroll
   for (int s = 0; s < kStages; ++s) issue(s);
-  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  __builtin_amdgcn_s_waitcnt(C::kWaitFirst);
   __builtin_amdgcn_s_barrier();
   Regs cur, nxt;
   read_stage(cur, 0);
@@ -684,17 +706,19 @@ static hipError_t launch_reg(const uint8_t* a_codes, const uint8_t* a_scales, co
   return hipGetLastError();
 }
 
+template <int WN>
 static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                              const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
                              bool out_f32, hipStream_t stream) {
-  p.tiles_m = (p.M + lds::BM - 1) / lds::BM;
-  p.tiles_n = (p.N + lds::BN - 1) / lds::BN;
-  const dim3 grid(p.tiles_m * p.tiles_n), block(lds::kThreads);
+  using C = LdsCfg<WN>;
+  p.tiles_m = (p.M + C::BM - 1) / C::BM;
+  p.tiles_n = (p.N + C::BN - 1) / C::BN;
+  const dim3 grid(p.tiles_m * p.tiles_n), block(C::kThreads);
   if (out_f32)
-    hipLaunchKernelGGL(gemm_lds_kernel<true>, grid, block, lds::kLdsBytes, stream, a_codes, a_scales, a_g,
+    hipLaunchKernelGGL((gemm_lds_kernel<WN, true>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
                        w_packed, w_g, y, p);
   else
-    hipLaunchKernelGGL(gemm_lds_kernel<false>, grid, block, lds::kLdsBytes, stream, a_codes, a_scales, a_g,
+    hipLaunchKernelGGL((gemm_lds_kernel<WN, false>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
                        w_packed, w_g, y, p);
   return hipGetLastError();
 }
@@ -732,7 +756,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
   if (aligned && M <= 32)
     return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
-  if (aligned) return launch_lds(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+  if (aligned) return launch_lds<2>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }
 
