@@ -71,6 +71,7 @@ struct GemmParams {
   uint32_t tiles_m, tiles_n;
   int n_seg;
   uint32_t seg_off[NVFP4_SEG_TABLE];
+  uint32_t y_pairs;          // bf16 output: y and ldy allow dword stores of column pairs
   // GDN gate epilogue (split-K kernel only): H b-columns, then H a-columns.
   const float* gate_a_log;
   const float* gate_dt_bias;
@@ -123,6 +124,13 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, ui
 // Index of the calling wave in its workgroup, in a scalar register.
 __device__ __forceinline__ uint32_t wave_index() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+// Two floats -> bf16 pair (lo, hi), round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, (bf16x2v){(__bf16)lo, (__bf16)hi});
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);     // finite inputs
@@ -152,6 +160,7 @@ __device__ __forceinline__ void store_tile(const floatx16 (&acc)[FM][FN], const 
                                            void* __restrict__ y, uint32_t m0, uint32_t n0, uint32_t r,
                                            uint32_t h) {
   const float ga = *a_g;
+  float alpha[FN];
 #pragma unroll
   for (int fb = 0; fb < FN; ++fb) {
     const uint32_t col = n0 + fb * 32 + r;
@@ -159,14 +168,47 @@ __device__ __forceinline__ void store_tile(const floatx16 (&acc)[FM][FN], const 
 #pragma unroll
     for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
     const float prod = ga * w_g[s];
-    const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+    alpha[fb] = prod == 0.0f ? 0.0f : 1.0f / prod;
+  }
+  if (!kF32Out && p.y_pairs && m0 + FM * 32 <= p.M && n0 + FN * 32 <= p.N) {
+    // Whole fragments in range, bf16 pairs aligned: lanes r and r ^ 1 trade
+    // halves so that each stores two adjacent columns of one row as one
+    // dword (even lane: rows 4g + {0, 1}; odd lane: rows 4g + {2, 3}).  The
+    // conversion is the hardware round to nearest even.
+    const bool odd = (r & 1u) != 0;
+    const uint32_t sel_a = odd ? 0x01000504u : 0x05040100u;   // low halves: (col even, col odd)
+    const uint32_t sel_b = odd ? 0x03020706u : 0x07060302u;   // high halves
+    const uint32_t col0 = n0 + (r & ~1u);
+#pragma unroll
+    for (int fa = 0; fa < FM; ++fa) {
+#pragma unroll
+      for (int fb = 0; fb < FN; ++fb) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const floatx16& v = acc[fa][fb];
+          const uint32_t pk0 = pack_bf16_rne(v[4 * g] * alpha[fb], v[4 * g + 1] * alpha[fb]);       // rows +0, +1
+          const uint32_t pk1 = pack_bf16_rne(v[4 * g + 2] * alpha[fb], v[4 * g + 3] * alpha[fb]);   // rows +2, +3
+          const uint32_t own = odd ? pk1 : pk0;
+          const uint32_t recv = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? pk0 : pk1), 0xB1, 0xF, 0xF, false);
+          const uint32_t row = m0 + fa * 32 + g * 8 + h * 4 + (odd ? 2u : 0u);
+          uint32_t* dst = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(y) + (size_t)row * p.ldy + col0 + fb * 32);
+          dst[0] = __builtin_amdgcn_perm(recv, own, sel_a);
+          *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(dst) + p.ldy) = __builtin_amdgcn_perm(recv, own, sel_b);
+        }
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int fb = 0; fb < FN; ++fb) {
+    const uint32_t col = n0 + fb * 32 + r;
 #pragma unroll
     for (int fa = 0; fa < FM; ++fa) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
         if (row < p.M && col < p.N) {
-          const float v = acc[fa][fb][i] * alpha;
+          const float v = acc[fa][fb][i] * alpha[fb];
           if (kF32Out)
             static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
           else
@@ -750,6 +792,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
                        int64_t ldy, bool out_f32, hipStream_t stream) {
   if (M == 0) return hipSuccess;
   GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
+  p.y_pairs = (ldy % 2 == 0) && (reinterpret_cast<uintptr_t>(y) % 4 == 0) ? 1u : 0u;
   const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   const bool aligned = (K % 64) == 0;
   if (aligned && N <= 96)
