@@ -1,7 +1,8 @@
 // Dynamic activation quantization to NVFP4 on gfx950 (paper, section 2
 // "NVFP4"; the run-time "A4" half of W4A4).
 //
-// Two launches on the caller's stream, no atomics and no memset:
+// Two launches on the caller's stream (one for activations of at most 4096
+// blocks, see act_quant_small_kernel), no atomics and no memset:
 //   1. amax_partial: each workgroup reduces |x| over a grid-strided share of
 //      X and writes one partial maximum to the workspace.  bf16 magnitudes
 //      order like unsigned integers, so the reduction is packed u16 max.
@@ -137,6 +138,68 @@ __global__ __launch_bounds__(kThreads) void act_quant_kernel(
 
 __global__ void write_zero_scale_kernel(float* g_enc) { *g_enc = 0.0f; }
 
+// Small activations (decode-shaped calls, a few tokens): one workgroup does
+// both passes, so the quantizer is one launch instead of two.  The amax is
+// the same order-free maximum; the blocks are quantized by the same code.
+constexpr int kSmallThreads = 1024;
+// Up to 4096 blocks (M * K <= 65536, e.g. a few tokens of width 5120) one
+// CU does the work faster than two launches spread over the chip.
+constexpr uint32_t kSmallMaxBlocks = 4096;
+
+template <bool kDynamic, bool kContig>
+__global__ __launch_bounds__(kSmallThreads) void act_quant_small_kernel(
+    const uint16_t* __restrict__ x, uint32_t n_blocks, uint32_t blocks_per_row, uint32_t ldx,
+    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ g_enc) {
+  __shared__ uint32_t lds[kSmallThreads / 64];
+  float g;
+  if (kDynamic) {
+    uint32_t m = 0;
+    for (uint32_t b = threadIdx.x; b < n_blocks; b += kSmallThreads) {
+      const uint4* src;
+      if (kContig) {
+        src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
+      } else {
+        uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
+        src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+      }
+      const uint4 d0 = src[0], d1 = src[1];
+      const uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+      const uint32_t a = __float_as_uint(block_amax(v));
+      m = m > a ? m : a;
+    }
+    // Workgroup maximum (16 waves).
+    m = wave_max_u32(m);
+    if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = lds[0];
+#pragma unroll
+    for (int w = 1; w < kSmallThreads / 64; ++w) m = m > lds[w] ? m : lds[w];
+    g = global_scale(__uint_as_float(m));
+    if (threadIdx.x == 0) *g_enc = g;
+  } else {
+    g = *g_enc;
+  }
+  const float gd6 = g * (1.0f / 6.0f);
+  for (uint32_t b = threadIdx.x; b < n_blocks; b += kSmallThreads) {
+    const uint4* src;
+    if (kContig) {
+      src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
+    } else {
+      uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
+      src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+    }
+    const uint4 d0 = src[0], d1 = src[1];
+    const uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    uint32_t c0, c1, sc;
+    if (g > kHugeScale)
+      sc = quantize_block<true, !kDynamic>(v, g, gd6, c0, c1);
+    else
+      sc = quantize_block<false, !kDynamic>(v, g, gd6, c0, c1);
+    reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
+    scales[b] = (uint8_t)sc;
+  }
+}
+
 static int grid_for(uint64_t work_items, int cap) {
   uint64_t g = (work_items + kThreads - 1) / kThreads;
   if (g > (uint64_t)cap) g = cap;
@@ -154,6 +217,18 @@ hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, ui
   const uint16_t* xp = static_cast<const uint16_t*>(x);
   const uint32_t n_vec = (uint32_t)(M * K / 8), vec_per_row = (uint32_t)(K / 8);
   const uint32_t n_blocks = (uint32_t)(M * K / 16), blocks_per_row = (uint32_t)(K / 16);
+  if (n_blocks <= kSmallMaxBlocks) {
+#define NVFP4_AQS(D, C)                                                                             \
+  hipLaunchKernelGGL((act_quant_small_kernel<D, C>), dim3(1), dim3(kSmallThreads), 0, stream, xp, n_blocks, \
+                     blocks_per_row, (uint32_t)ldx, codes, scales, g_enc)
+    if (dynamic) {
+      if (contig) NVFP4_AQS(true, true); else NVFP4_AQS(true, false);
+    } else {
+      if (contig) NVFP4_AQS(false, true); else NVFP4_AQS(false, false);
+    }
+#undef NVFP4_AQS
+    return hipGetLastError();
+  }
   int n_partial = 0;
   if (dynamic) {
     n_partial = grid_for(n_vec / 4, kActPartials);

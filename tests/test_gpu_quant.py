@@ -78,6 +78,28 @@ def test_act_quant_edge_cases():
     assert_act_matches(xb, g=np.float32(3e30))
 
 
+def test_act_quant_small_and_two_pass_paths_agree_on_edge_cases():
+    """Activations of at most 4096 blocks take the one-launch quantizer; the
+    same edge rows repeated past that size take the two-pass one."""
+    rng = np.random.default_rng(101)
+    x = rng.standard_normal((40, 96))
+    x[0] = 0.0
+    x[2, :16] *= 1e-4
+    x[2, 16] = 3e3
+    x[4, :] = -1e-35
+    xb = bits_of(x)
+    xb[3, ::3] = 0x8000
+    big = np.tile(xb, (20, 1))                    # 800 x 96: 4800 blocks
+    for t in (xb, big):
+        assert_act_matches(t)
+        assert_act_matches(t, ldx=128)
+        assert_act_matches(t, g=np.float32(2688.0 / 50.0))
+        assert_act_matches(t, g=np.float32(3e30))
+    z = np.zeros((4200, 16), dtype=np.uint16)     # denormal amax, two-pass path
+    z[1, 3] = 0x0001
+    assert_act_matches(z)
+
+
 def test_act_quant_special_tensors():
     assert_act_matches(np.zeros((8, 32), dtype=np.uint16))            # G = 0
     z = np.zeros((4, 16), dtype=np.uint16)
