@@ -266,7 +266,7 @@ def main():
         "roofline": {
             "bound": "mfma",
             "kernel": ("gemm_splitk_kernel<4, 2, 3> (tall-skinny NVFP4 GEMM + segment-scaled bf16 epilogue)"
-                       if cfg.n <= 96 else "gemm_lds_kernel<false> (NVFP4 GEMM + segment-scaled bf16 epilogue)"),
+                       if cfg.n <= 96 else "gemm_lds_kernel<LdsSquare, false> (256 x 256 NVFP4 GEMM + segment-scaled bf16 epilogue)"),
             "achieved": round(gemm_tflops, 2),
             "peak": MFMA_F16_PEAK_TFLOPS,
             "unit": "TFLOP/s",

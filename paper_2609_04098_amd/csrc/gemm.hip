@@ -19,28 +19,29 @@
 // exactly 4 bytes of packed codes under one block scale; see packed_layout.h
 // for the index map shared by the activation and the prepacked weight.
 //
-// Two kernels:
-//  * gemm_lds_kernel (K % 64 == 0, N > 96): 256 threads, 256 x 128 tile,
-//    wave tile 128 x 64 (4 x 2 accumulator fragments, 128 registers) so
-//    that two workgroups share a CU and every SIMD runs two waves: with one
-//    wave per SIMD an MFMA stream stalls issue, and the decode VALU work of
-//    one wave hides behind the MFMAs of the other.  Raw packed operands move
-//    global -> LDS with direct-to-LDS buffer loads through a 4-stage ring
-//    (each fragment loaded once per workgroup); each wave reads its raw
-//    fragments of the next chunk from LDS while it decodes and multiplies the
-//    current one.  One barrier per 64-deep chunk.  The loop body is a single
-//    basic block in which MFMAs, decode VALU, LDS reads and the DMA issue of
-//    a later chunk are interleaved (sched_group_barrier), so that the vector
+// Three kernels:
+//  * gemm_lds_kernel (K % 64 == 0, N > 96, M > 32; the prefill shapes): 256
+//    threads, 256 x 256 tile, wave tile 128 x 128 (4 x 4 accumulator
+//    fragments, 256 accumulator registers), one wave per SIMD; its own decode
+//    VALU co-issues with its MFMAs.  Raw packed operands move global -> LDS
+//    with direct-to-LDS buffer loads through a 4-stage ring (each fragment
+//    loaded once per workgroup, the chunk advance in the scalar offset of
+//    loop-invariant buffer descriptors); each wave reads its raw fragments of
+//    the next chunk from LDS while it decodes and multiplies the current one,
+//    and decodes the next chunk's first MFMA step beside the current chunk's
+//    last.  One barrier per 64-deep chunk.  The loop body is a single basic
+//    block in which MFMAs, decode VALU, LDS reads and the DMA issue of a
+//    later chunk are interleaved (sched_group_barrier), so that the vector
 //    memory queue and the VALU never stall the MFMA stream in bursts.
-//  * gemm_splitk_kernel (N <= 96, the tall-skinny gate projections): the
-//    output has too few 32 x 32 tiles for two waves per SIMD, so the four
-//    waves of a workgroup share one 64 x 96 tile and split its reduction;
-//    operands go straight from global memory to registers, three chunks in
-//    flight per wave, and the partial sums meet in LDS.
+//  * gemm_splitk_kernel (N <= 96, the tall-skinny gate projections; M <= 32,
+//    decode shapes): the output has too few 32 x 32 tiles to fill the chip,
+//    so the four waves of a workgroup share one tile and split its
+//    reduction, each streaming its chunks through a private LDS ring; the
+//    partial sums meet in LDS.
 //  * gemm_reg_kernel (K % 64 != 0, N > 96): operands go straight from global
 //    memory to registers one chunk ahead; per-block masking of the scales
 //    handles a K tail.
-// Both remap workgroups so that each XCD (its own L2) runs a contiguous,
+// All remap workgroups so that each XCD (its own L2) runs a contiguous,
 // M-grouped range of tiles; out-of-range rows/columns read zeros through the
 // buffer bounds and are not stored.
 #include <hip/hip_runtime.h>
@@ -114,11 +115,13 @@ __device__ __forceinline__ half8 decode8(uint32_t c, half2v s) {
 
 // Direct-to-LDS buffer loads: each lane's 16 (or 4) bytes at voffset land at
 // dst + 16 * lane (4 * lane); dst must be the same for the whole wave.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 16, voffset, 0, 0, 0);
+// The chunk advance goes in the scalar offset soffset; out-of-range per-lane
+// offsets (kOOB) read zeros.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset, uint32_t soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 16, voffset, soffset, 0, 0);
 }
-__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 4, voffset, 0, 0, 0);
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset, uint32_t soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 4, voffset, soffset, 0, 0);
 }
 
 // Index of the calling wave in its workgroup, in a scalar register.
@@ -228,14 +231,11 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
 constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt(0)
 }  // namespace lds
 
-// Workgroup shape of the LDS kernel: 2 x WN waves, each owning a 128 x 64
-// block of the output (4 x 2 accumulator fragments, 128 registers), so every
-// SIMD runs two waves.  WN = 2 (two 256 x 128 workgroups per CU) is the one
-// launched: WN = 4 (one 256 x 256 workgroup per CU, a third less operand
-// traffic per MFMA) measured 2-15% slower, as did rings of 3 or 5 stages.
-template <int WN_>
+// Workgroup shape of the LDS kernel: WM x WN waves, each owning an
+// FM x FN block of 32 x 32 accumulator fragments; kOcc workgroups per CU.
+template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_>
 struct LdsCfg {
-  static constexpr int WM = 2, WN = WN_, FM = 4, FN = 2;
+  static constexpr int WM = WM_, WN = WN_, FM = FM_, FN = FN_, kOcc = kOcc_;
   static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
   static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
@@ -249,20 +249,31 @@ struct LdsCfg {
   static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
   static constexpr int kLoadsPerWave = 2 * (kAPerWave + kBPerWave);
   static constexpr int kGroupM = 4;
-  static constexpr int kValuPerMfma = 5;                      // schedule: VALU slots after each MFMA
+  static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
+  static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
+  static constexpr int kLdsReads = 2 * (FM + FN);             // LDS reads per chunk and wave
   static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
   static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c+1 landed
   static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
+  static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
+  static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
 };
 
-template <int WN_, bool kF32Out>
-__global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
+// The launched shape: 256 x 256 workgroups of 2 x 2 waves, each wave a
+// 128 x 128 block (4 x 4 fragments, 256 accumulator registers), one
+// workgroup per CU.  Per chunk a wave decodes 8 fragments for 64 MFMAs
+// (4 VALU per MFMA); with 4 x 2 fragments and two waves per SIMD it was
+// 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
+// of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
+typedef LdsCfg<2, 2, 4, 4, 1, 6> LdsSquare;
+
+template <class C, bool kF32Out>
+__global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
                                                                    const uint8_t* __restrict__ a_scales,
                                                                    const float* __restrict__ a_g,
                                                                    const uint8_t* __restrict__ w_packed,
                                                                    const float* __restrict__ w_g,
                                                                    void* __restrict__ y, GemmParams p) {
-  using C = LdsCfg<WN_>;
   constexpr int WN = C::WN, FM = C::FM, FN = C::FN, BM = C::BM, BN = C::BN;
   constexpr int kA = C::kA, kB = C::kB, kSA = C::kSA, kSB = C::kSB, kStages = C::kStages;
   constexpr int kStageBytes = C::kStageBytes, kAPerWave = C::kAPerWave, kBPerWave = C::kBPerWave;
@@ -292,29 +303,27 @@ __global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(cons
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
 
-  auto chunk_rsrc = [&](const uint8_t* base, uint32_t bytes, uint32_t step, uint32_t kc) {
-    const uint32_t adv = kc * step;
-    const bool live = kc < p.chunks && adv < bytes;
-    return rsrc(base + (live ? adv : 0u), live ? bytes - adv : 0u);
-  };
-  // DMA of chunk kc into stage kc % kStages; chunks past the end read zeros.
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales, w_scale_bytes);
+  // DMA of chunk kc into stage kc % kStages.  The ring runs kStages - 1
+  // chunks past the end of K; those stages are never read, and re-load the
+  // last chunk so that every address stays inside its tensor.
   auto issue = [&](uint32_t kc) {
     uint8_t* st = smem + (kc % kStages) * kStageBytes;
-    const __amdgpu_buffer_rsrc_t ra = chunk_rsrc(a_codes, p.a_code_bytes, 32u, kc);
-    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(a_scales, p.a_scale_bytes, 4u, kc);
-    const __amdgpu_buffer_rsrc_t rb = chunk_rsrc(w_packed, p.w_scale_offset, 1024u, kc);
-    const __amdgpu_buffer_rsrc_t rbs = chunk_rsrc(w_scales, w_scale_bytes, 128u, kc);
+    const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
 #pragma unroll
     for (int i = 0; i < kAPerWave; ++i) {
       const uint32_t f = kAPerWave * wave + i;
-      dma16(ra, st + kA + f * 1024, a_off[i]);
-      dma4(rs, st + kSA + f * 256, as_off[i]);
+      dma16(ra, st + kA + f * 1024, a_off[i], kq * 32u);
+      dma4(rs, st + kSA + f * 256, as_off[i], kq * 4u);
     }
 #pragma unroll
     for (int i = 0; i < kBPerWave; ++i) {
       const uint32_t f = kBPerWave * wave + i;
-      dma16(rb, st + kB + f * 1024, b_off[i]);
-      dma4(rbs, st + kSB + f * 256, bs_off[i]);
+      dma16(rb, st + kB + f * 1024, b_off[i], kq * 1024u);
+      dma4(rbs, st + kSB + f * 256, bs_off[i], kq * 128u);
     }
   };
 
@@ -344,36 +353,46 @@ __global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(cons
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx16{};
 
+  // The decode of MFMA step 0 of chunk c + 1 runs beside the MFMAs of step 3
+  // of chunk c, so no iteration starts with a run of VALU work in front of
+  // its first MFMA (one wave per SIMD: nothing else would cover it).
+  half2v sA[FM], sB[FN];
+  half8 av[2][FM], bv[2][FN];
+  auto scales = [&](const Regs& R) {
+#pragma unroll
+    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(R.sa[f], 1.0f, false);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(R.sb[f], 1.0f, false);
+  };
+  // Decode MFMA step j (0..3) of R into buffer u; steps 0, 1 use the first
+  // block scale of the lane, steps 2, 3 the second.
+  auto decode_step = [&](const Regs& R, int j, int u) {
+#pragma unroll
+    for (int f = 0; f < FM; ++f)
+      av[u][f] = decode8((uint32_t)R.ca[f][j], j >> 1 ? __builtin_shufflevector(sA[f], sA[f], 1, 1)
+                                                      : __builtin_shufflevector(sA[f], sA[f], 0, 0));
+#pragma unroll
+    for (int f = 0; f < FN; ++f)
+      bv[u][f] = decode8((uint32_t)R.cb[f][j], j >> 1 ? __builtin_shufflevector(sB[f], sB[f], 1, 1)
+                                                      : __builtin_shufflevector(sB[f], sB[f], 0, 0));
+  };
   // One chunk: wait, barrier, DMA of chunk c + kStages, LDS reads of chunk
-  // c+1 into `next`, decode + MFMA of `cur`.
+  // c + 1 into `next`, decode + MFMA of `cur`.
   auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
-    __builtin_amdgcn_s_waitcnt(lds::kWaitLgkm0);
+    // Every LDS read of the previous iteration has been consumed by its
+    // decode, so after the barrier the stage of chunk c may be refilled.
     __builtin_amdgcn_s_waitcnt(C::kWaitNext);
     __builtin_amdgcn_s_barrier();
     issue(c + kStages);
     read_stage(next, c + 1);
-    // Both block scales of the lane (blocks 2h, 2h+1 of the chunk) as FP16.
-    half2v sA[FM], sB[FN];
-#pragma unroll
-    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sa[f], 1.0f, false);
-#pragma unroll
-    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cur.sb[f], 1.0f, false);
-    half8 av[2][FM], bv[2][FN];
-#pragma unroll
-    for (int f = 0; f < FM; ++f) av[0][f] = decode8((uint32_t)cur.ca[f][0], __builtin_shufflevector(sA[f], sA[f], 0, 0));
-#pragma unroll
-    for (int f = 0; f < FN; ++f) bv[0][f] = decode8((uint32_t)cur.cb[f][0], __builtin_shufflevector(sB[f], sB[f], 0, 0));
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int u = j & 1;
       if (j < 3) {
-        const int t = (j + 1) >> 1;
-#pragma unroll
-        for (int f = 0; f < FM; ++f)
-          av[u ^ 1][f] = decode8((uint32_t)cur.ca[f][j + 1], t ? __builtin_shufflevector(sA[f], sA[f], 1, 1) : __builtin_shufflevector(sA[f], sA[f], 0, 0));
-#pragma unroll
-        for (int f = 0; f < FN; ++f)
-          bv[u ^ 1][f] = decode8((uint32_t)cur.cb[f][j + 1], t ? __builtin_shufflevector(sB[f], sB[f], 1, 1) : __builtin_shufflevector(sB[f], sB[f], 0, 0));
+        decode_step(cur, j + 1, u ^ 1);
+      } else {
+        scales(next);
+        decode_step(next, 0, 0);
       }
 #pragma unroll
       for (int fa = 0; fa < FM; ++fa)
@@ -381,12 +400,15 @@ __global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(cons
         for (int fb = 0; fb < FN; ++fb)
           acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
     }
+    constexpr int kLdsEvery = (C::kMfma / 2) / C::kLdsReads;
+    constexpr int kDmaEvery = (3 * C::kMfma / 4) / C::kLoadsPerWave;
 #pragma unroll
-    for (int i = 0; i < 4 * FM * FN; ++i) {
+    for (int i = 0; i < C::kMfma; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
-      if (i % 2 == 1 && i < 24) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
-      if (i % 4 == 0 && i < 4 * C::kLoadsPerWave)
+      if (i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                     // LDS read
+      if (i % kDmaEvery == 0 && i / kDmaEvery < C::kLoadsPerWave)
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
     }
   };
@@ -397,6 +419,8 @@ __global__ __launch_bounds__(LdsCfg<WN_>::kThreads, 2) void gemm_lds_kernel(cons
   __builtin_amdgcn_s_barrier();
   Regs cur, nxt;
   read_stage(cur, 0);
+  scales(cur);
+  decode_step(cur, 0, 0);
   for (uint32_t c = 0; c < p.chunks; ++c) {
     step(c, cur, nxt);
     cur = nxt;
@@ -573,29 +597,26 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
   const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
 
-  auto chunk_rsrc = [&](const uint8_t* base, uint32_t bytes, uint32_t step, uint32_t kc) {
-    const uint32_t adv = kc * step;
-    const bool live = kc < p.chunks && adv < bytes;
-    return rsrc(base + (live ? adv : 0u), live ? bytes - adv : 0u);
-  };
-  // DMA of this wave's i-th chunk into stage i % kStages; chunks past the
-  // end of K read zeros.
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales, w_scale_bytes);
+  // DMA of this wave's i-th chunk into stage i % kStages.  Chunks past the
+  // end of K are never read; they re-load the last chunk so that every
+  // address stays inside its tensor.
   auto issue = [&](uint32_t i) {
     const uint32_t kc = wave + KS * i;
+    const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
     uint8_t* st = ring + (i % kStages) * kStageBytes;
-    const __amdgpu_buffer_rsrc_t ra = chunk_rsrc(a_codes, p.a_code_bytes, 32u, kc);
-    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(a_scales, p.a_scale_bytes, 4u, kc);
-    const __amdgpu_buffer_rsrc_t rb = chunk_rsrc(w_packed, p.w_scale_offset, 1024u, kc);
-    const __amdgpu_buffer_rsrc_t rbs = chunk_rsrc(w_scales, w_scale_bytes, 128u, kc);
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
-      dma16(ra, st + f * 1024, a_off[f]);
-      dma4(rs, st + kScaleBase + f * 256, as_off[f]);
+      dma16(ra, st + f * 1024, a_off[f], kq * 32u);
+      dma4(rs, st + kScaleBase + f * 256, as_off[f], kq * 4u);
     }
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
-      dma16(rb, st + (FM + f) * 1024, b_off[f]);
-      dma4(rbs, st + kScaleBase + (FM + f) * 256, bs_off[f]);
+      dma16(rb, st + (FM + f) * 1024, b_off[f], kq * 1024u);
+      dma4(rbs, st + kScaleBase + (FM + f) * 256, bs_off[f], kq * 128u);
     }
   };
 
@@ -748,19 +769,18 @@ static hipError_t launch_reg(const uint8_t* a_codes, const uint8_t* a_scales, co
   return hipGetLastError();
 }
 
-template <int WN>
+template <class C>
 static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                              const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
                              bool out_f32, hipStream_t stream) {
-  using C = LdsCfg<WN>;
   p.tiles_m = (p.M + C::BM - 1) / C::BM;
   p.tiles_n = (p.N + C::BN - 1) / C::BN;
   const dim3 grid(p.tiles_m * p.tiles_n), block(C::kThreads);
   if (out_f32)
-    hipLaunchKernelGGL((gemm_lds_kernel<WN, true>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
+    hipLaunchKernelGGL((gemm_lds_kernel<C, true>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
                        w_packed, w_g, y, p);
   else
-    hipLaunchKernelGGL((gemm_lds_kernel<WN, false>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
+    hipLaunchKernelGGL((gemm_lds_kernel<C, false>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
                        w_packed, w_g, y, p);
   return hipGetLastError();
 }
@@ -799,7 +819,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
   if (aligned && M <= 32)
     return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
-  if (aligned) return launch_lds<2>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+  if (aligned) return launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }
 

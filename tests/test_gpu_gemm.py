@@ -79,6 +79,7 @@ def test_gemm_tiny_workload():
     (32, 520, 5120, [0, 260, 520]),        # small-M split-K: 80 chunks over 8 waves, ragged N
     (1, 300, 1040, [0, 300]),              # small-M, one row, K % 64 != 0
     (17, 4100, 128, [0, 4000, 4100]),      # small-M, many column tiles, 2 chunks < 8 waves
+    (777, 1300, 384, [0, 500, 1300]),      # prefill path: 4 x 6 tiles of 256 x 256, ragged M and N
 ])
 def test_gemm_ragged_shapes(m, n, k, offs):
     rng = np.random.default_rng(m * 7 + n * 3 + k)
