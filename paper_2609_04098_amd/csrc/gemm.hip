@@ -47,6 +47,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "launch.h"
 #include "packed_layout.h"
 
@@ -233,28 +235,36 @@ constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt
 
 // Workgroup shape of the LDS kernel: WM x WN waves, each owning an
 // FM x FN block of 32 x 32 accumulator fragments; kOcc workgroups per CU.
-template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_>
+template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kSync_, int kStages_>
 struct LdsCfg {
   static constexpr int WM = WM_, WN = WN_, FM = FM_, FN = FN_, kOcc = kOcc_;
   static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
   static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
-  // One stage of the ring: raw codes (1 KB per fragment) and scales (256 B
-  // per fragment: one dword per lane) of one 64-deep chunk.
-  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 256;
-  static constexpr int kStageBytes = kSB + NFB * 256;
-  static constexpr int kStages = 4;
+  // One stage of the ring: raw codes (1 KB per fragment) and scales (one
+  // dword of 4 block scales per fragment row: 128 B per fragment) of one
+  // 64-deep chunk.
+  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 128;
+  static constexpr int kStageBytes = kSB + NFB * 128;
+  // kStages 64-deep stages in the ring; one barrier per kSync chunks.
+  static constexpr int kStages = kStages_, kSync = kSync_;
   static constexpr int kLdsBytes = kStages * kStageBytes;
+  // Chunks in flight: iteration i (chunks kSync i ...) refills the stages of
+  // chunks kDist ahead, whose previous chunks every wave consumed before
+  // the barrier that opens the iteration.
+  static constexpr int kDist = kStages - kSync + 1;
   // Each wave moves the same number of A and B fragments (codes + scales).
+  // The scales of two fragments (64 rows) move with one DMA.
   static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
-  static constexpr int kLoadsPerWave = 2 * (kAPerWave + kBPerWave);
+  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + (kAPerWave + kBPerWave) / 2;
   static constexpr int kGroupM = 4;
   static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
   static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
   static constexpr int kLdsReads = 2 * (FM + FN);             // LDS reads per chunk and wave
-  static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
-  static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c+1 landed
-  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
+  static constexpr int kWaitFirst = lds::vmcnt_imm((kDist - 1) * kLoadsPerWave);          // chunk 0 landed
+  static constexpr int kWaitNext = lds::vmcnt_imm((kDist - 1 - kSync) * kLoadsPerWave);   // chunks to c + kSync landed
+  static_assert(kSync >= 1 && kDist - 1 - kSync >= 0 && (kDist - 1) * kLoadsPerWave < 64, "ring depth");
+  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave % 2 == 0 && kBPerWave % 2 == 0, "load split");
   static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
   static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
 };
@@ -265,7 +275,7 @@ struct LdsCfg {
 // (4 VALU per MFMA); with 4 x 2 fragments and two waves per SIMD it was
 // 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
 // of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
-typedef LdsCfg<2, 2, 4, 4, 1, 6> LdsSquare;
+typedef LdsCfg<2, 2, 4, 4, 1, 6, 1, 4> LdsSquare;
 
 template <class C, bool kF32Out>
 __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
@@ -287,18 +297,29 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   // Per-lane offsets are fixed; the chunk advances the descriptors' base
   // (and shrinks their size) in scalar registers.  Rows >= M and tiles past
   // the packed weight get offsets beyond every descriptor: zeros.
-  uint32_t a_off[kAPerWave], as_off[kAPerWave], b_off[kBPerWave], bs_off[kBPerWave];
+  // Scale DMA of fragment pair j: lane l loads the scale dword of row l of
+  // the pair (A), or of row l % 32 of weight tile l / 32 of the pair (W).
+  uint32_t a_off[kAPerWave], as_off[kAPerWave / 2], b_off[kBPerWave], bs_off[kBPerWave / 2];
+  const uint32_t fa0 = kAPerWave * wave, fb0 = kBPerWave * wave;   // first fragment this wave loads
 #pragma unroll
   for (int i = 0; i < kAPerWave; ++i) {
-    const uint32_t row = tm * BM + (kAPerWave * wave + i) * 32 + r;
+    const uint32_t row = tm * BM + (fa0 + i) * 32 + r;
     a_off[i] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
-    as_off[i] = row < p.M ? row * (p.K >> 4) : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < kAPerWave / 2; ++j) {
+    const uint32_t row = tm * BM + (fa0 + 2 * j) * 32 + lane;
+    as_off[j] = row < p.M ? row * (p.K >> 4) : kOOB;
   }
 #pragma unroll
   for (int i = 0; i < kBPerWave; ++i) {
-    const uint32_t nt = tn * (BN / 32) + kBPerWave * wave + i;
+    const uint32_t nt = tn * (BN / 32) + fb0 + i;
     b_off[i] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
-    bs_off[i] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < kBPerWave / 2; ++j) {
+    const uint32_t nt = tn * (BN / 32) + fb0 + 2 * j + h;
+    bs_off[j] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
   }
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
@@ -314,36 +335,32 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
     uint8_t* st = smem + (kc % kStages) * kStageBytes;
     const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
 #pragma unroll
-    for (int i = 0; i < kAPerWave; ++i) {
-      const uint32_t f = kAPerWave * wave + i;
-      dma16(ra, st + kA + f * 1024, a_off[i], kq * 32u);
-      dma4(rs, st + kSA + f * 256, as_off[i], kq * 4u);
-    }
+    for (int i = 0; i < kAPerWave; ++i) dma16(ra, st + kA + (fa0 + i) * 1024, a_off[i], kq * 32u);
 #pragma unroll
-    for (int i = 0; i < kBPerWave; ++i) {
-      const uint32_t f = kBPerWave * wave + i;
-      dma16(rb, st + kB + f * 1024, b_off[i], kq * 1024u);
-      dma4(rbs, st + kSB + f * 256, bs_off[i], kq * 128u);
-    }
+    for (int j = 0; j < kAPerWave / 2; ++j) dma4(rs, st + kSA + (fa0 + 2 * j) * 128, as_off[j], kq * 4u);
+#pragma unroll
+    for (int i = 0; i < kBPerWave; ++i) dma16(rb, st + kB + (fb0 + i) * 1024, b_off[i], kq * 1024u);
+#pragma unroll
+    for (int j = 0; j < kBPerWave / 2; ++j) dma4(rbs, st + kSB + (fb0 + 2 * j) * 128, bs_off[j], kq * 128u);
   };
 
   struct Regs {
     int4v ca[FM], cb[FN];
     uint32_t sa[FM], sb[FN];   // low 16 bits: the lane's two block scales
   };
-  // Lanes r and 32 + r share their scale dword; each reads its own half
-  // (blocks 2h, 2h + 1 of the chunk).
+  // Lane (h, r) takes the half h of row r's scale dword (blocks 2h, 2h + 1
+  // of the chunk).
   auto read_stage = [&](Regs& R, uint32_t kc) {
     const uint8_t* st = smem + (kc % kStages) * kStageBytes;
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
-      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * 256 + lane * 4 + h * 2);
+      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * 128 + r * 4 + h * 2);
     }
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
-      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * 256 + lane * 4 + h * 2);
+      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * 128 + r * 4 + h * 2);
     }
   };
 
@@ -376,15 +393,13 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
       bv[u][f] = decode8((uint32_t)R.cb[f][j], j >> 1 ? __builtin_shufflevector(sB[f], sB[f], 1, 1)
                                                       : __builtin_shufflevector(sB[f], sB[f], 0, 0));
   };
-  // One chunk: wait, barrier, DMA of chunk c + kStages, LDS reads of chunk
-  // c + 1 into `next`, decode + MFMA of `cur`.
-  auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
-    // Every LDS read of the previous iteration has been consumed by its
-    // decode, so after the barrier the stage of chunk c may be refilled.
-    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
-    __builtin_amdgcn_s_barrier();
-    issue(c + kStages);
-    read_stage(next, c + 1);
+  // One chunk: LDS reads of chunk c + 1 into `next` (unless kRead is
+  // false: the last chunk's carried decode is never used), decode + MFMA of
+  // `cur`.  kDma: schedule slots for the DMA issued in front of it.
+  auto chunk = [&](uint32_t c, const Regs& cur, Regs& next, auto read_tag, auto dma_tag) {
+    constexpr bool kRead = decltype(read_tag)::value;
+    constexpr int kDma = decltype(dma_tag)::value;
+    if constexpr (kRead) read_stage(next, c + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int u = j & 1;
@@ -401,28 +416,48 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
           acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
     }
     constexpr int kLdsEvery = (C::kMfma / 2) / C::kLdsReads;
-    constexpr int kDmaEvery = (3 * C::kMfma / 4) / C::kLoadsPerWave;
+    constexpr int kDmaEvery = kDma ? (3 * C::kMfma / 4) / kDma : 1;
 #pragma unroll
     for (int i = 0; i < C::kMfma; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
-      if (i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
+      if (kRead && i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                     // LDS read
-      if (i % kDmaEvery == 0 && i / kDmaEvery < C::kLoadsPerWave)
+      if (kDma && i % kDmaEvery == 0 && i / kDmaEvery < kDma)
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
     }
   };
+  using kTrue = std::integral_constant<bool, true>;
+  using kFalse = std::integral_constant<bool, false>;
+  using kDmaSlots = std::integral_constant<int, C::kLoadsPerWave>;
+  using kNoDma = std::integral_constant<int, 0>;
 
 #pragma unroll
-  for (int s = 0; s < kStages; ++s) issue(s);
+  for (int s = 0; s < C::kDist; ++s) issue(s);
   __builtin_amdgcn_s_waitcnt(C::kWaitFirst);
   __builtin_amdgcn_s_barrier();
   Regs cur, nxt;
   read_stage(cur, 0);
   scales(cur);
   decode_step(cur, 0, 0);
-  for (uint32_t c = 0; c < p.chunks; ++c) {
-    step(c, cur, nxt);
+  const uint32_t groups = p.chunks / C::kSync;
+  for (uint32_t g = 0; g < groups; ++g) {
+    const uint32_t c0 = g * C::kSync;
+    // Every LDS read of earlier iterations has been consumed by its decode,
+    // so after the barrier the stages of chunks <= c0 may be refilled.
+    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int t = 0; t < C::kSync; ++t) issue(c0 + C::kDist + t);
+#pragma unroll
+    for (int t = 0; t < C::kSync; ++t) {
+      chunk(c0 + t, cur, nxt, kTrue{}, kDmaSlots{});
+      cur = nxt;
+    }
+  }
+  // A last chunk outside the groups: its data is in `cur` already.
+  for (uint32_t c = groups * C::kSync; c < p.chunks; ++c) {
+    chunk(c, cur, nxt, kFalse{}, kNoDma{});
     cur = nxt;
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
