@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* 
 
 // Grid-strided loop over 16-element blocks: 32 bytes of bf16 in, 8 bytes of
 // packed codes and 1 scale byte out per block.
-template <bool kContig, bool kHuge, bool kClamp>
+template <bool kContig, bool kHuge>
 __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, uint32_t n_blocks,
                                                 uint32_t blocks_per_row, uint32_t ldx,
                                                 uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -105,7 +105,7 @@ __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, 
     uint4 d0 = src[0], d1 = src[1];
     uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
     uint32_t c0, c1;
-    uint32_t sc = quantize_block<kHuge, kClamp>(v, g, gd6, c0, c1);
+    uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
     reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
     scales[b] = (uint8_t)sc;
   }
@@ -129,11 +129,11 @@ __global__ __launch_bounds__(kThreads) void act_quant_kernel(
   } else {
     g = *g_enc;
   }
-  // A dynamic G bounds |q| by 36; a static G needs the clamp.
+  // The scale path is chosen per tensor, uniformly across the launch.
   if (g > kHugeScale)
-    quantize_blocks<kContig, true, !kDynamic>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
+    quantize_blocks<kContig, true>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
   else
-    quantize_blocks<kContig, false, !kDynamic>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
+    quantize_blocks<kContig, false>(x, n_blocks, blocks_per_row, ldx, codes, scales, g);
 }
 
 __global__ void write_zero_scale_kernel(float* g_enc) { *g_enc = 0.0f; }
@@ -192,9 +192,9 @@ __global__ __launch_bounds__(kSmallThreads) void act_quant_small_kernel(
     const uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
     uint32_t c0, c1, sc;
     if (g > kHugeScale)
-      sc = quantize_block<true, !kDynamic>(v, g, gd6, c0, c1);
+      sc = quantize_block<true>(v, g, gd6, c0, c1);
     else
-      sc = quantize_block<false, !kDynamic>(v, g, gd6, c0, c1);
+      sc = quantize_block<false>(v, g, gd6, c0, c1);
     reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
     scales[b] = (uint8_t)sc;
   }

@@ -590,6 +590,18 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
 // while it decodes and multiplies the current one, and the partial sums meet
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
+// One stage of a split-K wave's ring: FM + FN raw code fragments (1 KB
+// each), then the scale dwords of the A fragments and of the W fragments,
+// two fragments (256 B) per scale DMA.
+template <int FM, int FN>
+struct SplitkStage {
+  static constexpr int kPairsA = (FM + 1) / 2, kPairsB = (FN + 1) / 2;
+  static constexpr int kScaleA = (FM + FN) * 1024;
+  static constexpr int kScaleB = kScaleA + kPairsA * 256;
+  static constexpr int kBytes = kScaleB + kPairsB * 256;
+  static constexpr int kLoads = FM + FN + kPairsA + kPairsB;
+};
+
 template <int KS, int FM, int FN, int kStages, bool kF32Out, bool kGate>
 __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* __restrict__ a_codes,
                                                              const uint8_t* __restrict__ a_scales,
@@ -598,10 +610,10 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
                                                              const float* __restrict__ w_g,
                                                              void* __restrict__ y, GemmParams p) {
   constexpr int BM = FM * 32, BN = FN * 32;
+  using L = SplitkStage<FM, FN>;
   constexpr int kFrags = FM + FN;
-  constexpr int kScaleBase = kFrags * 1024;                  // codes 1 KB, then scales 256 B per fragment
-  constexpr int kStageBytes = kFrags * 1280;
-  constexpr int kLoads = 2 * kFrags;                         // DMA loads per chunk and wave
+  constexpr int kScaleA = L::kScaleA, kScaleB = L::kScaleB, kStageBytes = L::kBytes;
+  constexpr int kLoads = L::kLoads;                          // DMA loads per chunk and wave
   constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoads);
   constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoads);
   static_assert(kStages >= 2 && (kStages - 1) * kLoads < 64, "memory counter range");
@@ -615,18 +627,29 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   const uint32_t m0 = tm * BM, n0 = tn * BN;
   uint8_t* ring = smem + wave * (kStages * kStageBytes);
 
-  uint32_t a_off[FM], as_off[FM], b_off[FN], bs_off[FN];
+  // Scale DMA of fragment pair j: lane l loads the scale dword of row l of
+  // the pair (A), or of row l % 32 of weight tile l / 32 of the pair (W);
+  // the missing second fragment of an odd count reads zeros.
+  uint32_t a_off[FM], as_off[L::kPairsA], b_off[FN], bs_off[L::kPairsB];
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
     const uint32_t row = m0 + f * 32 + r;
     a_off[f] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
-    as_off[f] = row < p.M ? row * (p.K >> 4) : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < L::kPairsA; ++j) {
+    const uint32_t row = m0 + 2 * j * 32 + lane;
+    as_off[j] = (2 * j + h < (uint32_t)FM && row < p.M) ? row * (p.K >> 4) : kOOB;
   }
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
     const uint32_t nt = (n0 >> 5) + f;
     b_off[f] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
-    bs_off[f] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < L::kPairsB; ++j) {
+    const uint32_t nt = (n0 >> 5) + 2 * j + h;
+    bs_off[j] = (2 * j + h < (uint32_t)FN && nt < p.w_tiles) ? nt * p.w_kc * 128u + r * 4u : kOOB;
   }
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
@@ -644,15 +667,13 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
     const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
     uint8_t* st = ring + (i % kStages) * kStageBytes;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      dma16(ra, st + f * 1024, a_off[f], kq * 32u);
-      dma4(rs, st + kScaleBase + f * 256, as_off[f], kq * 4u);
-    }
+    for (int f = 0; f < FM; ++f) dma16(ra, st + f * 1024, a_off[f], kq * 32u);
 #pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      dma16(rb, st + (FM + f) * 1024, b_off[f], kq * 1024u);
-      dma4(rbs, st + kScaleBase + (FM + f) * 256, bs_off[f], kq * 128u);
-    }
+    for (int j = 0; j < L::kPairsA; ++j) dma4(rs, st + kScaleA + j * 256, as_off[j], kq * 4u);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) dma16(rb, st + (FM + f) * 1024, b_off[f], kq * 1024u);
+#pragma unroll
+    for (int j = 0; j < L::kPairsB; ++j) dma4(rbs, st + kScaleB + j * 256, bs_off[j], kq * 128u);
   };
 
   struct Regs {
@@ -664,7 +685,7 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
 #pragma unroll
     for (int f = 0; f < kFrags; ++f) {
       R.c[f] = *(const int4v*)(st + f * 1024 + lane * 16);
-      R.s[f] = *(const uint32_t*)(st + kScaleBase + f * 256 + lane * 4);
+      R.s[f] = *(const uint32_t*)(st + (f < FM ? kScaleA + f * 128 : kScaleB + (f - FM) * 128) + r * 4);
     }
   };
 
@@ -767,7 +788,7 @@ static hipError_t launch_splitk(const uint8_t* a_codes, const uint8_t* a_scales,
                                 const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
                                 bool out_f32, bool gate, hipStream_t stream) {
   constexpr int BM = FM * 32, BN = FN * 32;
-  constexpr int kLds = KS * kStages * (FM + FN) * 1280;
+  constexpr int kLds = KS * kStages * SplitkStage<FM, FN>::kBytes;
   static_assert(kLds >= KS * 64 * 64, "the reduction reuses the rings");
   p.tiles_m = (p.M + BM - 1) / BM;
   p.tiles_n = (p.N + BN - 1) / BN;

@@ -53,7 +53,7 @@ __device__ __forceinline__ void norm_quant_row(const uint4* __restrict__ xr, con
       y_row[2 * b + 1] = make_uint4(v[4], v[5], v[6], v[7]);
     }
     uint32_t c0, c1;
-    const uint32_t sc = quantize_block<kHuge, true>(v, g, gd6, c0, c1);
+    const uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
     codes_row[b] = make_uint2(c0, c1);
     scales_row[b] = (uint8_t)sc;
   }

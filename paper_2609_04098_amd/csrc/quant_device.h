@@ -44,6 +44,15 @@ __device__ __forceinline__ int sign3(float e) {
   return r;
 }
 
+// max(|a|, |b|, |c|) of finite values in one v_max3_f32 (|.| as source
+// modifiers; written directly because the compiler adds canonicalizing
+// maxima around fmaxf).
+__device__ __forceinline__ float max3_abs(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, |%1|, |%2|, |%3|" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // Per-tensor global scale G = fl32(2688 / amax); 0 for amax = 0; overflow
 // saturates to the largest finite binary32 value.  The division is the
 // correctly rounded IEEE division (built with correctly rounded fp32 divide).
@@ -117,43 +126,54 @@ __device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
 // fma (abs/neg are free source modifiers), has the exact sign of |q| - |n|;
 // adding that sign to the bit pattern of n moves |n| by one ulp towards |q|
 // (for n = +-0, e >= 0).  The sign of x rides along in n, including -0.0.
-// kClamp (static scales): q is clamped to [-64, 64], beyond every midpoint,
-// so that an input beyond the calibrated range still saturates; with a
-// dynamic scale |q| <= 36 holds by construction.  kHuge: q formed as
+// Beyond the last midpoint (|q| > 20) every value saturates to 6, so a large
+// |q| needs no care: n S / 4 stays exact up to |n| = 2^20, and an infinite
+// q (an input far beyond a calibrated static scale) gives e = -inf and
+// w = +-FLT_MAX, which the conversion saturates.  kHuge: q formed as
 // (x G) (4 / S), which cannot overflow when G is near FLT_MAX.
-template <bool kHuge, bool kClamp>
+template <bool kHuge>
 __device__ __forceinline__ float e2m1_arg(float x, const ElemConsts& c) {
   float q = kHuge ? (x * c.g) * c.rq4 : x * c.grq;
-  if (kClamp) q = __builtin_amdgcn_fmed3f(q, -64.0f, 64.0f);
   float n = __builtin_rintf(q);
   float t = n * c.sq;                                          // exact
   int s = sign3(__builtin_fmaf(__builtin_fabsf(x), c.g, -__builtin_fabsf(t)));
   return __uint_as_float(__float_as_uint(n) + (uint32_t)s);
 }
 
-// Packed codes of 8 elements (4 dwords of bf16 pairs); element 2j goes to
-// the low nibble of byte j.  The conversion divides by 2^exponent(4.0) = 4
-// and rounds to nearest even with saturation.
-template <bool kHuge, bool kClamp>
-__device__ __forceinline__ uint32_t encode8(const uint32_t* d, const ElemConsts& k) {
+// Packed codes of 8 elements (binary32 values of 8 consecutive bf16
+// elements); element 2j goes to the low nibble of byte j.  The conversion
+// divides by 2^exponent(4.0) = 4 and rounds to nearest even with saturation.
+template <bool kHuge>
+__device__ __forceinline__ uint32_t encode8(const float* f, const ElemConsts& k) {
   uint32_t r = 0u;
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[0]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[0]), k), 4.0f, 0);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[1]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[1]), k), 4.0f, 1);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[2]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[2]), k), 4.0f, 2);
-  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge, kClamp>(bf16_lo(d[3]), k), e2m1_arg<kHuge, kClamp>(bf16_hi(d[3]), k), 4.0f, 3);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(f[0], k), e2m1_arg<kHuge>(f[1], k), 4.0f, 0);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(f[2], k), e2m1_arg<kHuge>(f[3], k), 4.0f, 1);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(f[4], k), e2m1_arg<kHuge>(f[5], k), 4.0f, 2);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, e2m1_arg<kHuge>(f[6], k), e2m1_arg<kHuge>(f[7], k), 4.0f, 3);
   return r;
 }
 
 // Quantize one block: 8 dwords of bf16 pairs -> 2 dwords of packed codes;
-// returns the E4M3 scale code.
-template <bool kHuge, bool kClamp>
+// returns the E4M3 scale code.  The block maximum is taken on the widened
+// values (|.| is a free source modifier of the three-input maximum); it is
+// exact, bf16 values being binary32 values, subnormals included.
+template <bool kHuge>
 __device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g, float gd6,
                                                    uint32_t& c0, uint32_t& c1) {
-  float amax_b = block_amax(v);
+  float f[16];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    f[2 * i] = bf16_lo(v[i]);
+    f[2 * i + 1] = bf16_hi(v[i]);
+  }
+  float amax_b = max3_abs(f[0], f[1], f[2]);
+#pragma unroll
+  for (int i = 3; i < 15; i += 2) amax_b = max3_abs(amax_b, f[i], f[i + 1]);
+  amax_b = max3_abs(amax_b, f[15], f[15]);
   uint32_t sc = scale_code(amax_b, g, gd6);
   ElemConsts k = elem_consts(g, scale_value(sc));
-  c0 = encode8<kHuge, kClamp>(v, k);
-  c1 = encode8<kHuge, kClamp>(v + 4, k);
+  c0 = encode8<kHuge>(f, k);
+  c1 = encode8<kHuge>(f + 8, k);
   return sc;
 }
 

@@ -101,10 +101,10 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
       const uint4* src = reinterpret_cast<const uint4*>(w + (size_t)n * ldw) + 2 * kb;
       uint4 d0 = src[0], d1 = src[1];
       uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-      // Static segment scales may be exceeded by the data: clamp always
-      // (the prepack is offline).
-      sc = g > kHugeScale ? quantize_block<true, true>(v, g, g * (1.0f / 6.0f), c0, c1)
-                          : quantize_block<false, true>(v, g, g * (1.0f / 6.0f), c0, c1);
+      // Static segment scales may be exceeded by the data; such elements
+      // saturate.
+      sc = g > kHugeScale ? quantize_block<true>(v, g, g * (1.0f / 6.0f), c0, c1)
+                          : quantize_block<false>(v, g, g * (1.0f / 6.0f), c0, c1);
     }
     *reinterpret_cast<uint2*>(packed + packed_code_offset(n, kb, kc_count)) = make_uint2(c0, c1);
     packed[scale_offset + packed_scale_offset(n, kb, kc_count)] = (uint8_t)sc;

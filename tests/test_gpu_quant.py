@@ -70,12 +70,16 @@ def test_act_quant_edge_cases():
     x[4, :] = -1e-35                        # tiny negatives
     xb = bits_of(x)
     xb[3, ::3] = 0x8000
+    xb[5, :16] = np.arange(1, 17, dtype=np.uint16) * 7        # bf16 subnormals (block max among them)
+    xb[5, 16:32] = 0x8000 | (np.arange(1, 17, dtype=np.uint16) * 5)   # negative subnormals
     assert_act_matches(xb)
     assert_act_matches(xb, ldx=128)         # strided rows
     # static scale from a smaller calibration amax: scales and codes saturate
     assert_act_matches(xb, g=np.float32(2688.0 / 50.0))
     assert_act_matches(xb, g=np.float32(1.0))
     assert_act_matches(xb, g=np.float32(3e30))
+    assert_act_matches(xb, g=np.float32(3.0e38))   # subnormal blocks get non-zero scales
+    assert_act_matches(xb, g=np.float32(1e20))     # most values far beyond the range: saturation
 
 
 def test_act_quant_small_and_two_pass_paths_agree_on_edge_cases():
