@@ -244,6 +244,34 @@ int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales,
                          const float* a_log, const float* dt_bias,
                          void* y, int64_t ldy, int y_dtype, void* stream);
 
+/*
+ * Activation quantization fused into a narrow GEMM (N <= 128: the
+ * tall-skinny gate projections; paper, section 2 for the format, section 6
+ * for the fused segments).  The result equals nvfp4_quantize_act followed
+ * by nvfp4_gemm: the activation is quantized by the same device code (the
+ * same codes, scales and G_A), and the GEMM sums in the same order as
+ * nvfp4_gemm at these shapes.  X is read once in static mode (twice in
+ * dynamic mode, whose global scale needs all of X first); the codes go to
+ * memory only if asked for.
+ *
+ *   x, M, K, ldx   bf16 activation, as for nvfp4_quantize_act.
+ *   a_g_enc        one device float: G_A, written (NVFP4_DYNAMIC) or read
+ *                  (NVFP4_STATIC), as for nvfp4_quantize_act.
+ *   workspace, workspace_bytes   as for nvfp4_quantize_act (dynamic mode).
+ *   w_packed, N, seg_offsets, n_seg, w_g_enc_seg, y, ldy, y_dtype
+ *                  as for nvfp4_gemm.
+ *   a_codes, a_scales   optional outputs ([M x K/2], [M x K/16] as written
+ *                  by nvfp4_quantize_act); both NULL or both set.
+ * Requirements: those of nvfp4_quantize_act and nvfp4_gemm; N > 128 or
+ * K % 64 != 0 gives NVFP4_EUNSUPPORTED.
+ */
+int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx,
+                        float* a_g_enc, int mode, void* workspace, size_t workspace_bytes,
+                        const void* w_packed, int64_t N,
+                        const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg,
+                        uint8_t* a_codes, uint8_t* a_scales,
+                        void* y, int64_t ldy, int y_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -206,6 +206,21 @@ static int grid_for(uint64_t work_items, int cap) {
   return g < 1 ? 1 : (int)g;
 }
 
+hipError_t launch_act_amax(const void* x, int64_t M, int64_t K, int64_t ldx, float* partial, int* n_partial,
+                           hipStream_t stream) {
+  const bool contig = (ldx == K);
+  const uint16_t* xp = static_cast<const uint16_t*>(x);
+  const uint32_t n_vec = (uint32_t)(M * K / 8), vec_per_row = (uint32_t)(K / 8);
+  *n_partial = grid_for(n_vec / 4, kActPartials);
+  if (contig)
+    hipLaunchKernelGGL(amax_partial_kernel<true>, dim3(*n_partial), dim3(kThreads), 0, stream, xp, n_vec,
+                       vec_per_row, (uint32_t)ldx, partial);
+  else
+    hipLaunchKernelGGL(amax_partial_kernel<false>, dim3(*n_partial), dim3(kThreads), 0, stream, xp, n_vec,
+                       vec_per_row, (uint32_t)ldx, partial);
+  return hipGetLastError();
+}
+
 hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
                             uint8_t* scales, float* g_enc, bool dynamic, float* partial,
                             hipStream_t stream) {
@@ -231,14 +246,7 @@ hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, ui
   }
   int n_partial = 0;
   if (dynamic) {
-    n_partial = grid_for(n_vec / 4, kActPartials);
-    if (contig)
-      hipLaunchKernelGGL(amax_partial_kernel<true>, dim3(n_partial), dim3(kThreads), 0, stream, xp,
-                         n_vec, vec_per_row, (uint32_t)ldx, partial);
-    else
-      hipLaunchKernelGGL(amax_partial_kernel<false>, dim3(n_partial), dim3(kThreads), 0, stream, xp,
-                         n_vec, vec_per_row, (uint32_t)ldx, partial);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_act_amax(x, M, K, ldx, partial, &n_partial, stream);
     if (e != hipSuccess) return e;
   }
   const int grid = grid_for(n_blocks, kActQuantGridCap);

@@ -256,4 +256,41 @@ int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const 
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 
+int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* a_g_enc, int mode,
+                        void* workspace, size_t workspace_bytes, const void* w_packed, int64_t N,
+                        const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg, uint8_t* a_codes,
+                        uint8_t* a_scales, void* y, int64_t ldy, int y_dtype, void* stream) {
+  if (mode != NVFP4_DYNAMIC && mode != NVFP4_STATIC) return NVFP4_EINVAL;
+  if (y_dtype != NVFP4_OUT_BF16 && y_dtype != NVFP4_OUT_F32) return NVFP4_EINVAL;
+  if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
+  if (ldy < N) return NVFP4_EINVAL;
+  if (M * K >= kI32Lim || N * K >= kI32Lim || M * ldy >= kI32Lim) return NVFP4_EINVAL;
+  if (nvfp4::packed_dims(N, K).bytes >= kI32Lim) return NVFP4_EINVAL;
+  if (!valid_segments(seg_offsets, n_seg, N)) return NVFP4_EINVAL;
+  if (a_g_enc == nullptr || w_g_enc_seg == nullptr || w_packed == nullptr) return NVFP4_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(a_g_enc) & 3u) || (reinterpret_cast<uintptr_t>(w_g_enc_seg) & 3u))
+    return NVFP4_EINVAL;
+  if (!aligned16(w_packed)) return NVFP4_EINVAL;
+  if ((a_codes == nullptr) != (a_scales == nullptr)) return NVFP4_EINVAL;
+  const bool dynamic = mode == NVFP4_DYNAMIC;
+  if (M > 0) {
+    if (ldx < K || ldx % 8 != 0 || M * ldx >= kI32Lim) return NVFP4_EINVAL;
+    if (x == nullptr || y == nullptr || !aligned16(x)) return NVFP4_EINVAL;
+    if (a_codes != nullptr && (!aligned16(a_codes) || !aligned16(a_scales))) return NVFP4_EINVAL;
+    const uintptr_t elem = y_dtype == NVFP4_OUT_F32 ? 4u : 2u;
+    if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
+  }
+  if (dynamic) {
+    if (workspace == nullptr || !aligned16(workspace)) return NVFP4_EINVAL;
+    if (workspace_bytes < nvfp4_quantize_act_workspace_bytes(M, K)) return NVFP4_EWORKSPACE;
+  }
+  if (N > 128 || K % 64 != 0) return NVFP4_EUNSUPPORTED;
+  int st = check_device();
+  if (st != NVFP4_OK) return st;
+  hipError_t e = nvfp4::launch_quant_gemm(x, M, K, ldx, a_g_enc, dynamic, static_cast<float*>(workspace), w_packed,
+                                          N, seg_offsets, n_seg, w_g_enc_seg, a_codes, a_scales, y, ldy,
+                                          y_dtype == NVFP4_OUT_F32, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
 }  // extern "C"

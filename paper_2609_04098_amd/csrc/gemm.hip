@@ -51,6 +51,7 @@
 
 #include "launch.h"
 #include "packed_layout.h"
+#include "quant_device.h"
 
 #define NVFP4_LDS __attribute__((address_space(3)))
 
@@ -590,6 +591,50 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
 // while it decodes and multiplies the current one, and the partial sums meet
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
+// Split-K epilogue: the KS waves' partial sums of each fragment meet in LDS
+// (part: KS x 64 floatx16), fragment f is summed in wave order
+// (deterministic) by wave f % KS, scaled by its column's segment scale (and
+// the GDN gate transform when kGate) and stored.
+template <int KS, int FM, int FN, bool kF32Out, bool kGate>
+__device__ __forceinline__ void splitk_epilogue(const floatx16 (&acc)[FM][FN], floatx16* part, const GemmParams& p,
+                                                float ga, const float* __restrict__ w_g, void* __restrict__ y,
+                                                uint32_t m0, uint32_t n0, uint32_t wave, uint32_t lane) {
+  const uint32_t r = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int fa = 0; fa < FM; ++fa) {
+#pragma unroll
+    for (int fb = 0; fb < FN; ++fb) {
+      const uint32_t owner = (fa * FN + fb) % KS;
+      part[wave * 64 + lane] = acc[fa][fb];
+      __syncthreads();
+      if (wave == owner) {
+        floatx16 sum = part[lane];
+#pragma unroll
+        for (int w = 1; w < KS; ++w) sum += part[w * 64 + lane];
+        const uint32_t col = n0 + fb * 32 + r;
+        int s = 0;
+#pragma unroll
+        for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+        const float prod = ga * w_g[s];
+        const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
+          if (row < p.M && col < p.N) {
+            float v = sum[i] * alpha;
+            if (kGate) v = gdn_gate(v, col, p);
+            if (kF32Out)
+              static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
+            else
+              static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
 // One stage of a split-K wave's ring: FM + FN raw code fragments (1 KB
 // each), then the scale dwords of the A fragments and of the W fragments,
 // two fragments (256 B) per scale DMA.
@@ -746,41 +791,171 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
 
-  floatx16* part = reinterpret_cast<floatx16*>(smem);       // [KS][64]
-  const float ga = *a_g;
+  splitk_epilogue<KS, FM, FN, kF32Out, kGate>(acc, reinterpret_cast<floatx16*>(smem), p, *a_g, w_g, y, m0, n0,
+                                              wave, lane);
+}
+
+// ------------------------------------------- fused quantize + tall-skinny GEMM
+//
+// For narrow outputs (N <= 128: the gate projections), the activation is
+// quantized inside the GEMM: each lane loads the 32 bf16 values it supplies
+// to the MFMA (row r, reduction indices [32h, 32h + 32) of the chunk: two
+// whole blocks), quantizes them with the same device code as the stand-alone
+// quantizer (so the codes are identical), optionally stores the codes and
+// scales, and feeds the decoded values to the MFMA; X is read once and the
+// codes never travel through memory.  Tile: 32 rows x FN fragments, the KS
+// waves of a workgroup split the reduction (wave w takes chunks w, w + KS,
+// ...), operands go straight to registers one chunk ahead, and the partial
+// sums meet in LDS (splitk_epilogue).  G_A is read (static) or formed from
+// the amax pass's partial maxima (dynamic; workgroup 0 writes it out), and
+// the epilogue uses the value, not the memory.  K % 64 == 0.
+struct QuantGemmArgs {
+  const uint16_t* x;
+  uint32_t x_bytes, ldx_bytes;
+  float* g_enc;
+  const float* partial;
+  uint32_t n_partial;
+  uint8_t* codes;
+  uint8_t* scales;
+};
+
+template <int KS, int FN, bool kDynamic, bool kF32Out, bool kCodes>
+__global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q, const uint8_t* __restrict__ w_packed,
+                                                            const float* __restrict__ w_g, void* __restrict__ y,
+                                                            GemmParams p) {
+  __shared__ floatx16 part[KS * 64];
+  __shared__ uint32_t red[KS];
+  const uint32_t lane = threadIdx.x & 63, wave = wave_index();
+  const uint32_t r = lane & 31, h = lane >> 5;
+  float g;
+  if (kDynamic) {
+    uint32_t m = 0;
+    for (uint32_t i = threadIdx.x; i < q.n_partial; i += KS * 64) {
+      const uint32_t v = __float_as_uint(q.partial[i]);
+      m = m > v ? m : v;                       // non-negative floats order as integers
+    }
 #pragma unroll
-  for (int fa = 0; fa < FM; ++fa) {
+    for (int off = 32; off > 0; off >>= 1) {
+      const uint32_t o = __shfl_xor(m, off, 64);
+      m = m > o ? m : o;
+    }
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    m = red[0];
 #pragma unroll
-    for (int fb = 0; fb < FN; ++fb) {
-      const uint32_t owner = (fa * FN + fb) % KS;
-      part[wave * 64 + lane] = acc[fa][fb];
-      __syncthreads();
-      if (wave == owner) {
-        floatx16 sum = part[lane];
+    for (int w = 1; w < KS; ++w) m = m > red[w] ? m : red[w];
+    g = global_scale(__uint_as_float(m));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *q.g_enc = g;
+  } else {
+    g = *q.g_enc;
+  }
+  const float gd6 = g * (1.0f / 6.0f);
+  uint32_t tm, tn;
+  tile_of<8>(p, tm, tn);
+  const uint32_t m0 = tm * 32, n0 = tn * (FN * 32);
+  const uint32_t row = m0 + r;
+
+  // Per-lane offsets; the chunk goes in the scalar offset.  Rows >= M read
+  // zeros (an all-zero block quantizes to zero codes and is not stored).
+  const __amdgpu_buffer_rsrc_t rx = rsrc(q.x, q.x_bytes);
+  const uint32_t x_off = row < p.M ? row * q.ldx_bytes + h * 64u : kOOB;
+  uint32_t b_off[FN], bs_off[FN];
 #pragma unroll
-        for (int w = 1; w < KS; ++w) sum += part[w * 64 + lane];
-        const uint32_t col = n0 + fb * 32 + r;
-        int s = 0;
+  for (int f = 0; f < FN; ++f) {
+    const uint32_t nt = (n0 >> 5) + f;
+    b_off[f] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+    bs_off[f] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u + h * 2u : kOOB;
+  }
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_packed + p.w_scale_offset, p.w_bytes - p.w_scale_offset);
+  const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+
+  struct Chunk {
+    int4v x[4];             // the lane's 32 bf16 values
+    int4v b[FN];
+    uint32_t sb[FN];        // low 16 bits: the lane's two weight block scales
+  };
+  auto load = [&](Chunk& c, uint32_t i) {
+    const uint32_t kc = wave + KS * i;
 #pragma unroll
-        for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
-        const float prod = ga * w_g[s];
-        const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+    for (int j = 0; j < 4; ++j) c.x[j] = __builtin_amdgcn_raw_buffer_load_b128(rx, x_off + 16u * j, kc * 128u, 0);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
-          if (row < p.M && col < p.N) {
-            float v = sum[i] * alpha;
-            if (kGate) v = gdn_gate(v, col, p);
-            if (kF32Out)
-              static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
-            else
-              static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
-          }
+    for (int f = 0; f < FN; ++f) {
+      c.b[f] = __builtin_amdgcn_raw_buffer_load_b128(rb, b_off[f], kc * 1024u, 0);
+      c.sb[f] = __builtin_amdgcn_raw_buffer_load_b16(rbs, bs_off[f], kc * 128u, 0);
+    }
+  };
+  floatx16 acc[1][FN];
+#pragma unroll
+  for (int f = 0; f < FN; ++f) acc[0][f] = floatx16{};
+
+  auto run = [&](auto huge_tag) {
+    constexpr bool kHuge = decltype(huge_tag)::value;
+    auto compute = [&](const Chunk& c, uint32_t i) {
+      const uint32_t kc = wave + KS * i;
+      const uint32_t v0[8] = {(uint32_t)c.x[0][0], (uint32_t)c.x[0][1], (uint32_t)c.x[0][2], (uint32_t)c.x[0][3],
+                              (uint32_t)c.x[1][0], (uint32_t)c.x[1][1], (uint32_t)c.x[1][2], (uint32_t)c.x[1][3]};
+      const uint32_t v1[8] = {(uint32_t)c.x[2][0], (uint32_t)c.x[2][1], (uint32_t)c.x[2][2], (uint32_t)c.x[2][3],
+                              (uint32_t)c.x[3][0], (uint32_t)c.x[3][1], (uint32_t)c.x[3][2], (uint32_t)c.x[3][3]};
+      uint32_t cd[4];
+      const uint32_t s0 = quantize_block<kHuge>(v0, g, gd6, cd[0], cd[1]);
+      const uint32_t s1 = quantize_block<kHuge>(v1, g, gd6, cd[2], cd[3]);
+      if (kCodes && row < p.M) {
+        *reinterpret_cast<uint4*>(q.codes + (size_t)row * (p.K >> 1) + kc * 32u + h * 16u) =
+            make_uint4(cd[0], cd[1], cd[2], cd[3]);
+        *reinterpret_cast<uint16_t*>(q.scales + (size_t)row * (p.K >> 4) + kc * 4u + h * 2u) =
+            (uint16_t)(s0 | (s1 << 8));
+      }
+      const half2v sa = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s0 | (s1 << 8), 1.0f, false);
+      half2v sb[FN];
+#pragma unroll
+      for (int f = 0; f < FN; ++f) sb[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(c.sb[f], 1.0f, false);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const half8 av = decode8(cd[j], j >> 1 ? __builtin_shufflevector(sa, sa, 1, 1)
+                                               : __builtin_shufflevector(sa, sa, 0, 0));
+#pragma unroll
+        for (int f = 0; f < FN; ++f) {
+          const half8 bv = decode8((uint32_t)c.b[f][j], j >> 1 ? __builtin_shufflevector(sb[f], sb[f], 1, 1)
+                                                                : __builtin_shufflevector(sb[f], sb[f], 0, 0));
+          acc[0][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, acc[0][f], 0, 0, 0);
         }
       }
-      __syncthreads();
+    };
+    Chunk cur, nxt;
+    if (n_mine > 0) load(cur, 0);
+    for (uint32_t i = 0; i < n_mine; ++i) {
+      if (i + 1 < n_mine) load(nxt, i + 1);
+      compute(cur, i);
+      cur = nxt;
     }
+  };
+  if (g > kHugeScale)
+    run(std::integral_constant<bool, true>{});
+  else
+    run(std::integral_constant<bool, false>{});
+  splitk_epilogue<KS, 1, FN, kF32Out, false>(acc, part, p, g, w_g, y, m0, n0, wave, lane);
+}
+
+template <int KS, int FN>
+static hipError_t launch_quant_gemm_fn(const QuantGemmArgs& q, bool dynamic, const uint8_t* w_packed,
+                                       const float* w_g, void* y, GemmParams p, bool out_f32,
+                                       hipStream_t stream) {
+  p.tiles_m = (p.M + 31) / 32;
+  p.tiles_n = (p.N + FN * 32 - 1) / (FN * 32);
+  const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
+#define NVFP4_QG(D, F32, CODES)                                                                       \
+  hipLaunchKernelGGL((quant_gemm_kernel<KS, FN, D, F32, CODES>), grid, block, 0, stream, q, w_packed, w_g, y, p)
+  const bool codes = q.codes != nullptr;
+  if (dynamic) {
+    if (out_f32) { if (codes) NVFP4_QG(true, true, true); else NVFP4_QG(true, true, false); }
+    else { if (codes) NVFP4_QG(true, false, true); else NVFP4_QG(true, false, false); }
+  } else {
+    if (out_f32) { if (codes) NVFP4_QG(false, true, true); else NVFP4_QG(false, true, false); }
+    else { if (codes) NVFP4_QG(false, false, true); else NVFP4_QG(false, false, false); }
   }
+#undef NVFP4_QG
+  return hipGetLastError();
 }
 
 template <int KS, int FM, int FN, int kStages>
@@ -891,6 +1066,34 @@ hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales
   p.gate_h = (uint32_t)H;
   return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, static_cast<const uint8_t*>(w_packed), w_g, y, p,
                                    out_f32, true, stream);
+}
+
+hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* g_enc, bool dynamic,
+                             float* partial, const void* w_packed, int64_t N, const int64_t* seg_offsets,
+                             int n_seg, const float* w_g, uint8_t* codes, uint8_t* scales, void* y, int64_t ldy,
+                             bool out_f32, hipStream_t stream) {
+  if (M == 0) {   // G as the quantizer writes it for an empty tensor
+    if (!dynamic) return hipSuccess;
+    return launch_act_quant(x, 0, K, ldx, codes, scales, g_enc, true, partial, stream);
+  }
+  QuantGemmArgs q{};
+  q.x = static_cast<const uint16_t*>(x);
+  q.x_bytes = (uint32_t)(M * ldx * 2);
+  q.ldx_bytes = (uint32_t)(ldx * 2);
+  q.g_enc = g_enc;
+  q.partial = partial;
+  q.codes = codes;
+  q.scales = scales;
+  if (dynamic) {
+    int n_partial = 0;
+    hipError_t e = launch_act_amax(x, M, K, ldx, partial, &n_partial, stream);
+    if (e != hipSuccess) return e;
+    q.n_partial = (uint32_t)n_partial;
+  }
+  GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
+  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
+  if (N <= 96) return launch_quant_gemm_fn<4, 3>(q, dynamic, wp, w_g, y, p, out_f32, stream);
+  return launch_quant_gemm_fn<4, 4>(q, dynamic, wp, w_g, y, p, out_f32, stream);
 }
 
 }  // namespace nvfp4

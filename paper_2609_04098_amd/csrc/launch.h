@@ -21,6 +21,11 @@ hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, ui
                             uint8_t* scales, float* g_enc, bool dynamic, float* partial,
                             hipStream_t stream);
 
+// Pass 1 of the dynamic quantizer: partial maxima of |x| into `partial`
+// (n_partial <= kActPartials values).
+hipError_t launch_act_amax(const void* x, int64_t M, int64_t K, int64_t ldx, float* partial, int* n_partial,
+                           hipStream_t stream);
+
 hipError_t launch_rmsnorm_quant(const void* x, int64_t M, int64_t K, int64_t ldx, const void* gamma,
                                 float eps, const float* g_enc, uint8_t* codes, uint8_t* scales, void* y,
                                 int64_t ldy, hipStream_t stream);
@@ -45,5 +50,10 @@ hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales
                                  int64_t M, int64_t K, const void* w_packed, int64_t H, const float* w_g,
                                  const float* a_log, const float* dt_bias, void* y, int64_t ldy,
                                  bool out_f32, hipStream_t stream);
+
+hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* g_enc, bool dynamic,
+                             float* partial, const void* w_packed, int64_t N, const int64_t* seg_offsets,
+                             int n_seg, const float* w_g, uint8_t* codes, uint8_t* scales, void* y, int64_t ldy,
+                             bool out_f32, hipStream_t stream);
 
 }  // namespace nvfp4

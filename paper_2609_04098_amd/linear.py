@@ -132,6 +132,32 @@ def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype
     return y
 
 
+def quantize_gemm(x, pw: PackedWeight, g=None, out_dtype=torch.bfloat16, out=None, act_out: QuantizedAct = None,
+                  workspace=None, stream=None):
+    """Act-quant fused into a narrow GEMM (N <= 128): y [M, N] equal to
+    gemm(quantize_act(x, g), pw).  Dynamic G unless ``g`` is given; the
+    activation codes/scales/G are written to ``act_out`` when it is given.
+    Returns (y, G as a device float32 [1])."""
+    m, k = x.shape
+    if k != pw.k:
+        raise ValueError("K mismatch between activation and weight")
+    dev = _dev(x)
+    y = out if out is not None else torch.empty((m, pw.n), dtype=out_dtype, device=dev)
+    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    gbuf = act_out.g if act_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
+    codes = act_out.codes if act_out is not None else None
+    scales = act_out.scales if act_out is not None else None
+    if g is None:
+        ws = act_workspace(m, k, dev) if workspace is None else workspace
+        _c.nvfp4_quantize_gemm(x, gbuf, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, _c.NVFP4_DYNAMIC, ws,
+                               codes, scales, kind, stream)
+    else:
+        gbuf.copy_(torch.as_tensor([float(g)], dtype=torch.float32))
+        _c.nvfp4_quantize_gemm(x, gbuf, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, _c.NVFP4_STATIC, None,
+                               codes, scales, kind, stream)
+    return y, gbuf
+
+
 def linear(x, pw: PackedWeight, out_dtype=torch.bfloat16):
     """y = x W^T through NVFP4 W4A4: dynamic act-quant, then the GEMM."""
     return gemm(quantize_act(x), pw, out_dtype)

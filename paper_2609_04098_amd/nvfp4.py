@@ -44,6 +44,8 @@ SIGNATURES = {
                                     _c_int64, _int, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
                           _c_int64, _int, _vp]),
+    "nvfp4_quantize_gemm": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _int, _vp, _sz, _vp, _c_int64,
+                                   _vp, _int, _vp, _vp, _vp, _vp, _c_int64, _int, _vp]),
 }
 
 _lib = None
@@ -178,3 +180,17 @@ def nvfp4_gemm_gdn_gates(a_codes, a_scales, a_g_enc, w_packed, H, w_g_enc_seg, a
                                     _ptr(w_g_enc_seg), _ptr(a_log), _ptr(dt_bias), _ptr(y), y.stride(0), y_dtype,
                                     _stream(stream))
     _check(st, "nvfp4_gemm_gdn_gates")
+
+
+def nvfp4_quantize_gemm(x, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y, mode=NVFP4_DYNAMIC,
+                        workspace=None, a_codes=None, a_scales=None, y_dtype=NVFP4_OUT_BF16, stream=None):
+    """Y [M, N] = quantize(x) then the segment-scaled GEMM, fused (N <= 128);
+    x bf16 [M, K] (row stride x.stride(0)); optional a_codes / a_scales
+    outputs."""
+    M, K = x.shape
+    offs, n_seg = _offsets(seg_offsets)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().nvfp4_quantize_gemm(_ptr(x), M, K, x.stride(0), _ptr(a_g_enc), mode, _ptr(workspace), ws_bytes,
+                                   _ptr(w_packed), N, offs, n_seg, _ptr(w_g_enc_seg), _ptr(a_codes),
+                                   _ptr(a_scales), _ptr(y), y.stride(0), y_dtype, _stream(stream))
+    _check(st, "nvfp4_quantize_gemm")

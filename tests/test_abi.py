@@ -184,3 +184,27 @@ def test_gdn_gates_rejects_bad_arguments():
     assert call(y=None) == C.NVFP4_EINVAL
     assert call(dtype=3) == C.NVFP4_EINVAL
     assert call(K=80) == C.NVFP4_EUNSUPPORTED       # the gate epilogue needs K % 64 == 0
+
+
+def test_quantize_gemm_rejects_bad_arguments():
+    f = C.lib().nvfp4_quantize_gemm
+    offs = _offs([0, 48, 96])
+
+    def call(M=16, K=128, ldx=128, mode=C.NVFP4_STATIC, ws=None, wsb=0, N=96, segs=offs, nseg=2, codes=None,
+             scales=None, y=FAKE, ldy=96, dtype=0, x=FAKE, g=FAKE):
+        return f(x, M, K, ldx, g, mode, ws, wsb, FAKE, N, segs, nseg, FAKE, codes, scales, y, ldy, dtype, None)
+    assert call(mode=5) == C.NVFP4_EINVAL
+    assert call(K=40) == C.NVFP4_EINVAL              # K % 16 != 0
+    assert call(ldx=120) == C.NVFP4_EINVAL           # ldx < K
+    assert call(ldx=132) == C.NVFP4_EINVAL           # ldx % 8 != 0
+    assert call(x=FAKE + 8) == C.NVFP4_EINVAL        # x not 16-byte aligned
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert call(codes=FAKE) == C.NVFP4_EINVAL        # codes without scales
+    assert call(codes=FAKE + 4, scales=FAKE) == C.NVFP4_EINVAL
+    assert call(ldy=95) == C.NVFP4_EINVAL
+    assert call(nseg=3) == C.NVFP4_EINVAL            # table ends past N
+    assert call(y=FAKE + 1) == C.NVFP4_EINVAL
+    assert call(mode=C.NVFP4_DYNAMIC) == C.NVFP4_EINVAL          # no workspace
+    assert call(mode=C.NVFP4_DYNAMIC, ws=FAKE, wsb=4) == C.NVFP4_EWORKSPACE
+    assert call(N=160, segs=_offs([0, 160]), nseg=1, ldy=160) == C.NVFP4_EUNSUPPORTED   # N > 128
+    assert call(K=80, ldx=80) == C.NVFP4_EUNSUPPORTED             # K % 64 != 0
