@@ -238,6 +238,30 @@ def main():
         gates_avg = float(np.mean([a.elapsed_time(b) for a, b in gev]))
         gates = {"avg_ms": round(gates_avg, 4), "plain_gemm_avg_ms": round(gemm_avg, 4),
                  "note": "GEMM with the GDN gate transform (beta | alpha) in the epilogue"}
+    fused = None
+    if cfg.n <= 128 and cfg.k % 64 == 0:
+        # Narrow outputs: act-quant fused into the GEMM (one launch after the
+        # amax pass; X read once with a calibrated scale), timed like the step.
+        g_static = aq.g.clone()
+        gf = torch.empty(1, dtype=torch.float32, device=dev)
+        res = {}
+        for name, mode in (("dynamic", C.NVFP4_DYNAMIC), ("static", C.NVFP4_STATIC)):
+            gb = gf if mode == C.NVFP4_DYNAMIC else g_static
+            wsp = ws if mode == C.NVFP4_DYNAMIC else None
+            call = lambda: C.nvfp4_quantize_gemm(x, gb, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, mode, wsp,
+                                                 stream=stream)
+            for _ in range(args.warmup):
+                call()
+            fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+            for i in range(args.steps):
+                fev[i][0].record(stream)
+                call()
+                fev[i][1].record(stream)
+            torch.cuda.synchronize()
+            f_ms = float(np.mean([a.elapsed_time(b) for a, b in fev]))
+            res[name] = {"avg_ms": round(f_ms, 4), "tflops_incl_act_quant": round(flops / (f_ms * 1e-3) / 1e12, 2)}
+        fused = dict(res, note="nvfp4_quantize_gemm: act-quant fused into the narrow GEMM (dynamic: amax pass + "
+                               "one fused launch; static: one launch with the calibrated G); not part of value")
     aq_static_gbs = aq_bytes / (aq_static_avg * 1e-3) / 1e9
     norm_gbs = aq_bytes / (norm_avg * 1e-3) / 1e9
     log("step %.3f ms (events %.3f), act-quant %.3f ms, GEMM %.3f ms" % (
@@ -293,6 +317,7 @@ def main():
             "note": "RMSNorm fused with the static-scale quantizer, one pass, X from HBM (median); not part of value",
         },
         "gdn_gates": gates,
+        "fused_quantize_gemm": fused,
         "frac_of_mxfp4_peak": round(value / MXFP4_PEAK_TFLOPS, 4),
         "prepack_ms": round(prepack_ms, 3),
         "gemm_source_sha256_16": gemm_source_hash(),

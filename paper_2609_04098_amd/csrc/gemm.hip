@@ -819,7 +819,7 @@ struct QuantGemmArgs {
   uint8_t* scales;
 };
 
-template <int KS, int FN, bool kDynamic, bool kF32Out, bool kCodes>
+template <int KS, int FM, int FN, int kDepth, bool kDynamic, bool kF32Out, bool kCodes>
 __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q, const uint8_t* __restrict__ w_packed,
                                                             const float* __restrict__ w_g, void* __restrict__ y,
                                                             GemmParams p) {
@@ -852,13 +852,17 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
   const float gd6 = g * (1.0f / 6.0f);
   uint32_t tm, tn;
   tile_of<8>(p, tm, tn);
-  const uint32_t m0 = tm * 32, n0 = tn * (FN * 32);
-  const uint32_t row = m0 + r;
+  const uint32_t m0 = tm * (FM * 32), n0 = tn * (FN * 32);
 
   // Per-lane offsets; the chunk goes in the scalar offset.  Rows >= M read
   // zeros (an all-zero block quantizes to zero codes and is not stored).
   const __amdgpu_buffer_rsrc_t rx = rsrc(q.x, q.x_bytes);
-  const uint32_t x_off = row < p.M ? row * q.ldx_bytes + h * 64u : kOOB;
+  uint32_t x_off[FM];
+#pragma unroll
+  for (int f = 0; f < FM; ++f) {
+    const uint32_t row = m0 + f * 32 + r;
+    x_off[f] = row < p.M ? row * q.ldx_bytes + h * 64u : kOOB;
+  }
   uint32_t b_off[FN], bs_off[FN];
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
@@ -871,81 +875,107 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
   const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
 
   struct Chunk {
-    int4v x[4];             // the lane's 32 bf16 values
+    int4v x[FM][4];         // per fragment, the lane's 32 bf16 values
     int4v b[FN];
     uint32_t sb[FN];        // low 16 bits: the lane's two weight block scales
   };
   auto load = [&](Chunk& c, uint32_t i) {
     const uint32_t kc = wave + KS * i;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c.x[j] = __builtin_amdgcn_raw_buffer_load_b128(rx, x_off + 16u * j, kc * 128u, 0);
+    for (int f = 0; f < FM; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        c.x[f][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, x_off[f] + 16u * j, kc * 128u, 0);
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       c.b[f] = __builtin_amdgcn_raw_buffer_load_b128(rb, b_off[f], kc * 1024u, 0);
       c.sb[f] = __builtin_amdgcn_raw_buffer_load_b16(rbs, bs_off[f], kc * 128u, 0);
     }
   };
-  floatx16 acc[1][FN];
+  floatx16 acc[FM][FN];
 #pragma unroll
-  for (int f = 0; f < FN; ++f) acc[0][f] = floatx16{};
+  for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+    for (int fb = 0; fb < FN; ++fb) acc[fa][fb] = floatx16{};
 
   auto run = [&](auto huge_tag) {
     constexpr bool kHuge = decltype(huge_tag)::value;
     auto compute = [&](const Chunk& c, uint32_t i) {
       const uint32_t kc = wave + KS * i;
-      const uint32_t v0[8] = {(uint32_t)c.x[0][0], (uint32_t)c.x[0][1], (uint32_t)c.x[0][2], (uint32_t)c.x[0][3],
-                              (uint32_t)c.x[1][0], (uint32_t)c.x[1][1], (uint32_t)c.x[1][2], (uint32_t)c.x[1][3]};
-      const uint32_t v1[8] = {(uint32_t)c.x[2][0], (uint32_t)c.x[2][1], (uint32_t)c.x[2][2], (uint32_t)c.x[2][3],
-                              (uint32_t)c.x[3][0], (uint32_t)c.x[3][1], (uint32_t)c.x[3][2], (uint32_t)c.x[3][3]};
-      uint32_t cd[4];
-      const uint32_t s0 = quantize_block<kHuge>(v0, g, gd6, cd[0], cd[1]);
-      const uint32_t s1 = quantize_block<kHuge>(v1, g, gd6, cd[2], cd[3]);
-      if (kCodes && row < p.M) {
-        *reinterpret_cast<uint4*>(q.codes + (size_t)row * (p.K >> 1) + kc * 32u + h * 16u) =
-            make_uint4(cd[0], cd[1], cd[2], cd[3]);
-        *reinterpret_cast<uint16_t*>(q.scales + (size_t)row * (p.K >> 4) + kc * 4u + h * 2u) =
-            (uint16_t)(s0 | (s1 << 8));
+      uint32_t cd[FM][4];
+      half2v sa[FM];
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        const uint32_t v0[8] = {(uint32_t)c.x[f][0][0], (uint32_t)c.x[f][0][1], (uint32_t)c.x[f][0][2],
+                                (uint32_t)c.x[f][0][3], (uint32_t)c.x[f][1][0], (uint32_t)c.x[f][1][1],
+                                (uint32_t)c.x[f][1][2], (uint32_t)c.x[f][1][3]};
+        const uint32_t v1[8] = {(uint32_t)c.x[f][2][0], (uint32_t)c.x[f][2][1], (uint32_t)c.x[f][2][2],
+                                (uint32_t)c.x[f][2][3], (uint32_t)c.x[f][3][0], (uint32_t)c.x[f][3][1],
+                                (uint32_t)c.x[f][3][2], (uint32_t)c.x[f][3][3]};
+        const uint32_t s0 = quantize_block<kHuge>(v0, g, gd6, cd[f][0], cd[f][1]);
+        const uint32_t s1 = quantize_block<kHuge>(v1, g, gd6, cd[f][2], cd[f][3]);
+        const uint32_t row = m0 + f * 32 + r;
+        if (kCodes && row < p.M) {
+          *reinterpret_cast<uint4*>(q.codes + (size_t)row * (p.K >> 1) + kc * 32u + h * 16u) =
+              make_uint4(cd[f][0], cd[f][1], cd[f][2], cd[f][3]);
+          *reinterpret_cast<uint16_t*>(q.scales + (size_t)row * (p.K >> 4) + kc * 4u + h * 2u) =
+              (uint16_t)(s0 | (s1 << 8));
+        }
+        sa[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s0 | (s1 << 8), 1.0f, false);
       }
-      const half2v sa = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s0 | (s1 << 8), 1.0f, false);
       half2v sb[FN];
 #pragma unroll
       for (int f = 0; f < FN; ++f) sb[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(c.sb[f], 1.0f, false);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const half8 av = decode8(cd[j], j >> 1 ? __builtin_shufflevector(sa, sa, 1, 1)
-                                               : __builtin_shufflevector(sa, sa, 0, 0));
+        half8 bv[FN];
 #pragma unroll
-        for (int f = 0; f < FN; ++f) {
-          const half8 bv = decode8((uint32_t)c.b[f][j], j >> 1 ? __builtin_shufflevector(sb[f], sb[f], 1, 1)
-                                                                : __builtin_shufflevector(sb[f], sb[f], 0, 0));
-          acc[0][f] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, acc[0][f], 0, 0, 0);
+        for (int f = 0; f < FN; ++f)
+          bv[f] = decode8((uint32_t)c.b[f][j], j >> 1 ? __builtin_shufflevector(sb[f], sb[f], 1, 1)
+                                                      : __builtin_shufflevector(sb[f], sb[f], 0, 0));
+#pragma unroll
+        for (int fa = 0; fa < FM; ++fa) {
+          const half8 av = decode8(cd[fa][j], j >> 1 ? __builtin_shufflevector(sa[fa], sa[fa], 1, 1)
+                                                     : __builtin_shufflevector(sa[fa], sa[fa], 0, 0));
+#pragma unroll
+          for (int fb = 0; fb < FN; ++fb)
+            acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv[fb], acc[fa][fb], 0, 0, 0);
         }
       }
     };
-    Chunk cur, nxt;
-    if (n_mine > 0) load(cur, 0);
-    for (uint32_t i = 0; i < n_mine; ++i) {
-      if (i + 1 < n_mine) load(nxt, i + 1);
-      compute(cur, i);
-      cur = nxt;
+    // Register ring of kDepth + 1 chunks: chunk i + kDepth is loaded while
+    // chunk i is computed (the loop unrolled over the ring's slots).
+    constexpr int kRing = kDepth + 1;
+    Chunk ring[kRing];
+#pragma unroll
+    for (int u = 0; u < kDepth; ++u)
+      if ((uint32_t)u < n_mine) load(ring[u], u);
+    for (uint32_t i = 0; i < n_mine; i += kRing) {
+#pragma unroll
+      for (int u = 0; u < kRing; ++u) {
+        if (i + u < n_mine) {
+          if (i + u + kDepth < n_mine) load(ring[(u + kDepth) % kRing], i + u + kDepth);
+          compute(ring[u], i + u);
+        }
+      }
     }
   };
   if (g > kHugeScale)
     run(std::integral_constant<bool, true>{});
   else
     run(std::integral_constant<bool, false>{});
-  splitk_epilogue<KS, 1, FN, kF32Out, false>(acc, part, p, g, w_g, y, m0, n0, wave, lane);
+  splitk_epilogue<KS, FM, FN, kF32Out, false>(acc, part, p, g, w_g, y, m0, n0, wave, lane);
 }
 
-template <int KS, int FN>
+template <int KS, int FM, int FN, int kDepth>
 static hipError_t launch_quant_gemm_fn(const QuantGemmArgs& q, bool dynamic, const uint8_t* w_packed,
                                        const float* w_g, void* y, GemmParams p, bool out_f32,
                                        hipStream_t stream) {
-  p.tiles_m = (p.M + 31) / 32;
+  p.tiles_m = (p.M + FM * 32 - 1) / (FM * 32);
   p.tiles_n = (p.N + FN * 32 - 1) / (FN * 32);
   const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
-#define NVFP4_QG(D, F32, CODES)                                                                       \
-  hipLaunchKernelGGL((quant_gemm_kernel<KS, FN, D, F32, CODES>), grid, block, 0, stream, q, w_packed, w_g, y, p)
+#define NVFP4_QG(D, F32, CODES)                                                                           \
+  hipLaunchKernelGGL((quant_gemm_kernel<KS, FM, FN, kDepth, D, F32, CODES>), grid, block, 0, stream, q, w_packed, w_g, y, p)
   const bool codes = q.codes != nullptr;
   if (dynamic) {
     if (out_f32) { if (codes) NVFP4_QG(true, true, true); else NVFP4_QG(true, true, false); }
@@ -1092,8 +1122,8 @@ hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, f
   }
   GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
   const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
-  if (N <= 96) return launch_quant_gemm_fn<4, 3>(q, dynamic, wp, w_g, y, p, out_f32, stream);
-  return launch_quant_gemm_fn<4, 4>(q, dynamic, wp, w_g, y, p, out_f32, stream);
+  if (N <= 96) return launch_quant_gemm_fn<4, 2, 3, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
+  return launch_quant_gemm_fn<4, 1, 4, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
 }
 
 }  // namespace nvfp4
