@@ -592,43 +592,56 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
 // Split-K epilogue: the KS waves' partial sums of each fragment meet in LDS
-// (part: KS x 64 floatx16), fragment f is summed in wave order
-// (deterministic) by wave f % KS, scaled by its column's segment scale (and
-// the GDN gate transform when kGate) and stored.
+// (part: KS x 64 floatx16) and are summed in wave order (deterministic).
+// Plain outputs: fragment f is summed and stored by wave f % KS.  With the
+// GDN gate transform (kGate), whose transcendentals dominate the epilogue,
+// every wave takes 16 / KS of each lane's 16 accumulator entries of every
+// fragment instead, so that all waves share that arithmetic.  Each value is
+// scaled by its column's segment scale.
 template <int KS, int FM, int FN, bool kF32Out, bool kGate>
 __device__ __forceinline__ void splitk_epilogue(const floatx16 (&acc)[FM][FN], floatx16* part, const GemmParams& p,
                                                 float ga, const float* __restrict__ w_g, void* __restrict__ y,
                                                 uint32_t m0, uint32_t n0, uint32_t wave, uint32_t lane) {
+  static_assert(16 % KS == 0, "entries per wave");
+  constexpr int kPer = 16 / KS;
   const uint32_t r = lane & 31, h = lane >> 5;
+  const float* partf = reinterpret_cast<const float*>(part);
+  auto store = [&](float v, uint32_t row, uint32_t col) {
+    if (row < p.M && col < p.N) {
+      if (kGate) v = gdn_gate(v, col, p);
+      if (kF32Out)
+        static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
+      else
+        static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
+    }
+  };
 #pragma unroll
   for (int fa = 0; fa < FM; ++fa) {
 #pragma unroll
     for (int fb = 0; fb < FN; ++fb) {
-      const uint32_t owner = (fa * FN + fb) % KS;
       part[wave * 64 + lane] = acc[fa][fb];
       __syncthreads();
-      if (wave == owner) {
+      const uint32_t col = n0 + fb * 32 + r;
+      int s = 0;
+#pragma unroll
+      for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+      const float prod = ga * w_g[s];
+      const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+      if (kGate) {
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+          const uint32_t i = wave * kPer + e;               // accumulator entry of this wave
+          float sum = partf[lane * 16 + i];
+#pragma unroll
+          for (int w = 1; w < KS; ++w) sum += partf[(w * 64 + lane) * 16 + i];
+          store(sum * alpha, m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
+        }
+      } else if (wave == (uint32_t)((fa * FN + fb) % KS)) {
         floatx16 sum = part[lane];
 #pragma unroll
         for (int w = 1; w < KS; ++w) sum += part[w * 64 + lane];
-        const uint32_t col = n0 + fb * 32 + r;
-        int s = 0;
 #pragma unroll
-        for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
-        const float prod = ga * w_g[s];
-        const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const uint32_t row = m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
-          if (row < p.M && col < p.N) {
-            float v = sum[i] * alpha;
-            if (kGate) v = gdn_gate(v, col, p);
-            if (kF32Out)
-              static_cast<float*>(y)[(size_t)row * p.ldy + col] = v;
-            else
-              static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(v);
-          }
-        }
+        for (int i = 0; i < 16; ++i) store(sum[i] * alpha, m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
       }
       __syncthreads();
     }
