@@ -73,6 +73,7 @@ struct GemmParams {
   uint32_t w_tiles;         // Np / 32
   uint32_t a_code_bytes, a_scale_bytes, w_bytes;
   uint32_t tiles_m, tiles_n;
+  uint32_t n_off;            // first output column of tile column 0 (LDS kernel; multiple of 32)
   int n_seg;
   uint32_t seg_off[NVFP4_SEG_TABLE];
   uint32_t y_pairs;          // bf16 output: y and ldy allow dword stores of column pairs
@@ -242,11 +243,19 @@ struct LdsCfg {
   static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
   static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
-  // One stage of the ring: raw codes (1 KB per fragment) and scales (one
-  // dword of 4 block scales per fragment row: 128 B per fragment) of one
-  // 64-deep chunk.
-  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * 128;
-  static constexpr int kStageBytes = kSB + NFB * 128;
+  // Each wave moves the same number of A and B fragments (codes + scales).
+  static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
+  // Scales: one dword of 4 block scales per fragment row and chunk.  With an
+  // even count per wave, one DMA moves the scales of two fragments (64
+  // distinct rows, 128 B per fragment slot); with an odd count, one DMA per
+  // fragment (both half-waves load the same 32 rows; 256 B slots).
+  static constexpr bool kPairA = kAPerWave % 2 == 0, kPairB = kBPerWave % 2 == 0;
+  static constexpr int kSFA = kPairA ? 128 : 256, kSFB = kPairB ? 128 : 256;
+  static constexpr int kSDmaA = kPairA ? kAPerWave / 2 : kAPerWave, kSDmaB = kPairB ? kBPerWave / 2 : kBPerWave;
+  // One stage of the ring: raw codes (1 KB per fragment), then the scale
+  // slots, of one 64-deep chunk.
+  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * kSFA;
+  static constexpr int kStageBytes = kSB + NFB * kSFB;
   // kStages 64-deep stages in the ring; one barrier per kSync chunks.
   static constexpr int kStages = kStages_, kSync = kSync_;
   static constexpr int kLdsBytes = kStages * kStageBytes;
@@ -254,10 +263,7 @@ struct LdsCfg {
   // chunks kDist ahead, whose previous chunks every wave consumed before
   // the barrier that opens the iteration.
   static constexpr int kDist = kStages - kSync + 1;
-  // Each wave moves the same number of A and B fragments (codes + scales).
-  // The scales of two fragments (64 rows) move with one DMA.
-  static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
-  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + (kAPerWave + kBPerWave) / 2;
+  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + kSDmaA + kSDmaB;
   static constexpr int kGroupM = 4;
   static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
   static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
@@ -265,7 +271,7 @@ struct LdsCfg {
   static constexpr int kWaitFirst = lds::vmcnt_imm((kDist - 1) * kLoadsPerWave);          // chunk 0 landed
   static constexpr int kWaitNext = lds::vmcnt_imm((kDist - 1 - kSync) * kLoadsPerWave);   // chunks to c + kSync landed
   static_assert(kSync >= 1 && kDist - 1 - kSync >= 0 && (kDist - 1) * kLoadsPerWave < 64, "ring depth");
-  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave % 2 == 0 && kBPerWave % 2 == 0, "load split");
+  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
   static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
   static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
 };
@@ -277,6 +283,10 @@ struct LdsCfg {
 // 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
 // of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
 typedef LdsCfg<2, 2, 4, 4, 1, 6, 1, 4> LdsSquare;
+// 256 x 128 workgroups of 2 x 2 waves with 4 x 2 fragments, two per CU: the
+// tail of a launch whose last round of square tiles would be at most half
+// full (see launch_gemm).
+typedef LdsCfg<2, 2, 4, 2, 2, 5, 1, 4> LdsTall;
 
 template <class C, bool kF32Out>
 __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
@@ -298,28 +308,29 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   // Per-lane offsets are fixed; the chunk advances the descriptors' base
   // (and shrinks their size) in scalar registers.  Rows >= M and tiles past
   // the packed weight get offsets beyond every descriptor: zeros.
-  // Scale DMA of fragment pair j: lane l loads the scale dword of row l of
-  // the pair (A), or of row l % 32 of weight tile l / 32 of the pair (W).
-  uint32_t a_off[kAPerWave], as_off[kAPerWave / 2], b_off[kBPerWave], bs_off[kBPerWave / 2];
+  // Scale DMA j: lane (h, r) loads the scale dword of row r of fragment
+  // j * 2 + h of the wave's pair (paired), or of fragment j (single).
+  uint32_t a_off[kAPerWave], as_off[C::kSDmaA], b_off[kBPerWave], bs_off[C::kSDmaB];
   const uint32_t fa0 = kAPerWave * wave, fb0 = kBPerWave * wave;   // first fragment this wave loads
+  const uint32_t nt0 = (p.n_off >> 5) + tn * (BN / 32);             // first weight tile of the tile
 #pragma unroll
   for (int i = 0; i < kAPerWave; ++i) {
     const uint32_t row = tm * BM + (fa0 + i) * 32 + r;
     a_off[i] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
   }
 #pragma unroll
-  for (int j = 0; j < kAPerWave / 2; ++j) {
-    const uint32_t row = tm * BM + (fa0 + 2 * j) * 32 + lane;
+  for (int j = 0; j < C::kSDmaA; ++j) {
+    const uint32_t row = tm * BM + (fa0 + (C::kPairA ? 2 * j + h : j)) * 32 + r;
     as_off[j] = row < p.M ? row * (p.K >> 4) : kOOB;
   }
 #pragma unroll
   for (int i = 0; i < kBPerWave; ++i) {
-    const uint32_t nt = tn * (BN / 32) + fb0 + i;
+    const uint32_t nt = nt0 + fb0 + i;
     b_off[i] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
   }
 #pragma unroll
-  for (int j = 0; j < kBPerWave / 2; ++j) {
-    const uint32_t nt = tn * (BN / 32) + fb0 + 2 * j + h;
+  for (int j = 0; j < C::kSDmaB; ++j) {
+    const uint32_t nt = nt0 + fb0 + (C::kPairB ? 2 * j + h : j);
     bs_off[j] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
   }
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
@@ -338,11 +349,13 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
 #pragma unroll
     for (int i = 0; i < kAPerWave; ++i) dma16(ra, st + kA + (fa0 + i) * 1024, a_off[i], kq * 32u);
 #pragma unroll
-    for (int j = 0; j < kAPerWave / 2; ++j) dma4(rs, st + kSA + (fa0 + 2 * j) * 128, as_off[j], kq * 4u);
+    for (int j = 0; j < C::kSDmaA; ++j)
+      dma4(rs, st + kSA + (fa0 + (C::kPairA ? 2 * j : j)) * C::kSFA, as_off[j], kq * 4u);
 #pragma unroll
     for (int i = 0; i < kBPerWave; ++i) dma16(rb, st + kB + (fb0 + i) * 1024, b_off[i], kq * 1024u);
 #pragma unroll
-    for (int j = 0; j < kBPerWave / 2; ++j) dma4(rbs, st + kSB + (fb0 + 2 * j) * 128, bs_off[j], kq * 128u);
+    for (int j = 0; j < C::kSDmaB; ++j)
+      dma4(rbs, st + kSB + (fb0 + (C::kPairB ? 2 * j : j)) * C::kSFB, bs_off[j], kq * 128u);
   };
 
   struct Regs {
@@ -356,12 +369,12 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
-      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * 128 + r * 4 + h * 2);
+      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * C::kSFA + r * 4 + h * 2);
     }
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
-      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * 128 + r * 4 + h * 2);
+      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * C::kSFB + r * 4 + h * 2);
     }
   };
 
@@ -463,7 +476,7 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
   __builtin_amdgcn_s_waitcnt(0x0F70);
-  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, tm * BM + wm * FM * 32, tn * BN + wn * FN * 32, r, h);
+  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, tm * BM + wm * FM * 32, p.n_off + tn * BN + wn * FN * 32, r, h);
 }
 
 // ------------------------------------------------------------- register path
@@ -1043,12 +1056,14 @@ static hipError_t launch_reg(const uint8_t* a_codes, const uint8_t* a_scales, co
   return hipGetLastError();
 }
 
+// Output columns [n_begin, n_end) (n_begin a multiple of 32).
 template <class C>
 static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                              const uint8_t* w_packed, const float* w_g, void* y, GemmParams p,
-                             bool out_f32, hipStream_t stream) {
+                             uint32_t n_begin, uint32_t n_end, bool out_f32, hipStream_t stream) {
+  p.n_off = n_begin;
   p.tiles_m = (p.M + C::BM - 1) / C::BM;
-  p.tiles_n = (p.N + C::BN - 1) / C::BN;
+  p.tiles_n = (n_end - n_begin + C::BN - 1) / C::BN;
   const dim3 grid(p.tiles_m * p.tiles_n), block(C::kThreads);
   if (out_f32)
     hipLaunchKernelGGL((gemm_lds_kernel<C, true>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
@@ -1057,6 +1072,19 @@ static hipError_t launch_lds(const uint8_t* a_codes, const uint8_t* a_scales, co
     hipLaunchKernelGGL((gemm_lds_kernel<C, false>), grid, block, C::kLdsBytes, stream, a_codes, a_scales, a_g,
                        w_packed, w_g, y, p);
   return hipGetLastError();
+}
+
+// Compute units of the current device (cached per device).
+static uint32_t cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cached[dev] = n;
+  }
+  return (uint32_t)cached[dev];
 }
 
 static GemmParams gemm_params(int64_t M, int64_t K, int64_t N, const int64_t* seg_offsets, int n_seg,
@@ -1093,7 +1121,23 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     return launch_splitk<4, 2, 3, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
   if (aligned && M <= 32)
     return launch_splitk<4, 1, 2, 3>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, false, stream);
-  if (aligned) return launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, stream);
+  if (aligned) {
+    // Square tiles fill whole rounds of one workgroup per CU.  When the last
+    // round would be at most half full and its tiles make whole tile
+    // columns, those columns run as a second launch of 256 x 128 tiles (two
+    // per CU), which takes about half a round instead of a full one.
+    const uint32_t tiles_m = (uint32_t)((M + LdsSquare::BM - 1) / LdsSquare::BM);
+    const uint32_t tiles_n = (uint32_t)((N + LdsSquare::BN - 1) / LdsSquare::BN);
+    const uint32_t n_cu = cu_count();
+    const uint32_t rem = n_cu ? (tiles_m * tiles_n) % n_cu : 0;
+    if (rem != 0 && rem <= n_cu / 2 && rem % tiles_m == 0 && rem / tiles_m < tiles_n) {
+      const uint32_t n_split = (tiles_n - rem / tiles_m) * LdsSquare::BN;
+      hipError_t e = launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, n_split, out_f32, stream);
+      if (e != hipSuccess) return e;
+      return launch_lds<LdsTall>(a_codes, a_scales, a_g, wp, w_g, y, p, n_split, (uint32_t)N, out_f32, stream);
+    }
+    return launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, (uint32_t)N, out_f32, stream);
+  }
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
 }
 

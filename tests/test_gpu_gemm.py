@@ -87,6 +87,24 @@ def test_gemm_ragged_shapes(m, n, k, offs):
     check_small(x, w, offs, what="%dx%dx%d" % (m, n, k))
 
 
+def test_gemm_tail_columns_as_narrow_tiles():
+    # 2 x 130 tiles of 256 x 256: on a 256-CU device the 4 tiles past two
+    # full rounds (two tile columns) run as 256 x 128 tiles in a second
+    # launch; ragged M and N inside that tail.  Every element is checked.
+    rng = np.random.default_rng(304)
+    m, n, k = 300, 129 * 256 + 100, 128
+    x, w = _xw(rng, m, n, k)
+    offs = [0, 20000, 33000, n]
+    y32, y16, _, _ = run_gpu(x, w, offs)
+    xp, xs, gx = OQ.quantize_tensor(x)
+    wp, ws, gw = OQ.quantize_segments(w, offs)
+    y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs)
+    r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "tail split")
+    np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_of(y32.contiguous()))
+
+
 def test_gemm_strided_output():
     rng = np.random.default_rng(300)
     x, w = _xw(rng, 70, 136, 256)
