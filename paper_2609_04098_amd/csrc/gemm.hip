@@ -237,7 +237,7 @@ constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt
 
 // Workgroup shape of the LDS kernel: WM x WN waves, each owning an
 // FM x FN block of 32 x 32 accumulator fragments; kOcc workgroups per CU.
-template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kSync_, int kStages_>
+template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kStages_>
 struct LdsCfg {
   static constexpr int WM = WM_, WN = WN_, FM = FM_, FN = FN_, kOcc = kOcc_;
   static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
@@ -256,21 +256,19 @@ struct LdsCfg {
   // slots, of one 64-deep chunk.
   static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * kSFA;
   static constexpr int kStageBytes = kSB + NFB * kSFB;
-  // kStages 64-deep stages in the ring; one barrier per kSync chunks.
-  static constexpr int kStages = kStages_, kSync = kSync_;
+  // kStages 64-deep stages in the ring; iteration c refills the stage of
+  // chunk c (consumed by every wave before the barrier that opens the
+  // iteration) with chunk c + kStages.
+  static constexpr int kStages = kStages_;
   static constexpr int kLdsBytes = kStages * kStageBytes;
-  // Chunks in flight: iteration i (chunks kSync i ...) refills the stages of
-  // chunks kDist ahead, whose previous chunks every wave consumed before
-  // the barrier that opens the iteration.
-  static constexpr int kDist = kStages - kSync + 1;
   static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + kSDmaA + kSDmaB;
   static constexpr int kGroupM = 4;
   static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
   static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
   static constexpr int kLdsReads = 2 * (FM + FN);             // LDS reads per chunk and wave
-  static constexpr int kWaitFirst = lds::vmcnt_imm((kDist - 1) * kLoadsPerWave);          // chunk 0 landed
-  static constexpr int kWaitNext = lds::vmcnt_imm((kDist - 1 - kSync) * kLoadsPerWave);   // chunks to c + kSync landed
-  static_assert(kSync >= 1 && kDist - 1 - kSync >= 0 && (kDist - 1) * kLoadsPerWave < 64, "ring depth");
+  static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
+  static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c + 1 landed
+  static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerWave < 64, "ring depth");
   static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
   static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
   static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
@@ -282,11 +280,11 @@ struct LdsCfg {
 // (4 VALU per MFMA); with 4 x 2 fragments and two waves per SIMD it was
 // 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
 // of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
-typedef LdsCfg<2, 2, 4, 4, 1, 6, 1, 4> LdsSquare;
+typedef LdsCfg<2, 2, 4, 4, 1, 6, 4> LdsSquare;
 // 256 x 128 workgroups of 2 x 2 waves with 4 x 2 fragments, two per CU: the
 // tail of a launch whose last round of square tiles would be at most half
 // full (see launch_gemm).
-typedef LdsCfg<2, 2, 4, 2, 2, 5, 1, 4> LdsTall;
+typedef LdsCfg<2, 2, 4, 2, 2, 5, 4> LdsTall;
 
 template <class C, bool kF32Out>
 __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
@@ -407,13 +405,16 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
       bv[u][f] = decode8((uint32_t)R.cb[f][j], j >> 1 ? __builtin_shufflevector(sB[f], sB[f], 1, 1)
                                                       : __builtin_shufflevector(sB[f], sB[f], 0, 0));
   };
-  // One chunk: LDS reads of chunk c + 1 into `next` (unless kRead is
-  // false: the last chunk's carried decode is never used), decode + MFMA of
-  // `cur`.  kDma: schedule slots for the DMA issued in front of it.
-  auto chunk = [&](uint32_t c, const Regs& cur, Regs& next, auto read_tag, auto dma_tag) {
-    constexpr bool kRead = decltype(read_tag)::value;
-    constexpr int kDma = decltype(dma_tag)::value;
-    if constexpr (kRead) read_stage(next, c + 1);
+  // One chunk: wait until chunk c + 1 has landed, barrier, DMA of chunk
+  // c + kStages into the stage of chunk c, LDS reads of chunk c + 1 into
+  // `next`, decode + MFMA of `cur`.
+  auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
+    // Every LDS read of the previous iteration has been consumed by its
+    // decode, so after the barrier the stage of chunk c may be refilled.
+    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
+    __builtin_amdgcn_s_barrier();
+    issue(c + kStages);
+    read_stage(next, c + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int u = j & 1;
@@ -429,49 +430,31 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
         for (int fb = 0; fb < FN; ++fb)
           acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
     }
+    // LDS reads spread over the first half of the chunk, DMA issues over the
+    // first three quarters.
     constexpr int kLdsEvery = (C::kMfma / 2) / C::kLdsReads;
-    constexpr int kDmaEvery = kDma ? (3 * C::kMfma / 4) / kDma : 1;
+    constexpr int kDmaEvery = (3 * C::kMfma / 4) / C::kLoadsPerWave;
 #pragma unroll
     for (int i = 0; i < C::kMfma; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
-      if (kRead && i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
+      if (i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                     // LDS read
-      if (kDma && i % kDmaEvery == 0 && i / kDmaEvery < kDma)
+      if (i % kDmaEvery == 0 && i / kDmaEvery < C::kLoadsPerWave)
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
     }
   };
-  using kTrue = std::integral_constant<bool, true>;
-  using kFalse = std::integral_constant<bool, false>;
-  using kDmaSlots = std::integral_constant<int, C::kLoadsPerWave>;
-  using kNoDma = std::integral_constant<int, 0>;
 
 #pragma unroll
-  for (int s = 0; s < C::kDist; ++s) issue(s);
+  for (int s = 0; s < kStages; ++s) issue(s);
   __builtin_amdgcn_s_waitcnt(C::kWaitFirst);
   __builtin_amdgcn_s_barrier();
   Regs cur, nxt;
   read_stage(cur, 0);
   scales(cur);
   decode_step(cur, 0, 0);
-  const uint32_t groups = p.chunks / C::kSync;
-  for (uint32_t g = 0; g < groups; ++g) {
-    const uint32_t c0 = g * C::kSync;
-    // Every LDS read of earlier iterations has been consumed by its decode,
-    // so after the barrier the stages of chunks <= c0 may be refilled.
-    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
-    __builtin_amdgcn_s_barrier();
-#pragma unroll
-    for (int t = 0; t < C::kSync; ++t) issue(c0 + C::kDist + t);
-#pragma unroll
-    for (int t = 0; t < C::kSync; ++t) {
-      chunk(c0 + t, cur, nxt, kTrue{}, kDmaSlots{});
-      cur = nxt;
-    }
-  }
-  // A last chunk outside the groups: its data is in `cur` already.
-  for (uint32_t c = groups * C::kSync; c < p.chunks; ++c) {
-    chunk(c, cur, nxt, kFalse{}, kNoDma{});
+  for (uint32_t c = 0; c < p.chunks; ++c) {
+    step(c, cur, nxt);
     cur = nxt;
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
