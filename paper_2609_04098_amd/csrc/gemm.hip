@@ -237,9 +237,13 @@ constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt
 
 // Workgroup shape of the LDS kernel: WM x WN waves, each owning an
 // FM x FN block of 32 x 32 accumulator fragments; kOcc workgroups per CU.
-template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kStages_>
+template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kStages_, bool kSuper_ = false>
 struct LdsCfg {
   static constexpr int WM = WM_, WN = WN_, FM = FM_, FN = FN_, kOcc = kOcc_;
+  // kSuper (K % 256 == 0): the scales of 4 consecutive chunks move together,
+  // one 16-byte DMA per fragment pair (a row's 4 scale dwords are
+  // contiguous), into two alternating scale "super-stages" beside the ring.
+  static constexpr bool kSuper = kSuper_;
   static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
   static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
   static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
@@ -255,19 +259,31 @@ struct LdsCfg {
   // One stage of the ring: raw codes (1 KB per fragment), then the scale
   // slots, of one 64-deep chunk.
   static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * kSFA;
-  static constexpr int kStageBytes = kSB + NFB * kSFB;
+  static constexpr int kStageBytes = kSuper ? kSA : kSB + NFB * kSFB;
+  // A super-stage: per A fragment [32 rows][4 chunks][4 B] (512 B), then per
+  // W fragment [4 chunks][32 rows][4 B] (512 B, the packed order).
+  static constexpr int kSuperB = NFA * 512, kSuperBytes = kSuperB + NFB * 512;
   // kStages 64-deep stages in the ring; iteration c refills the stage of
   // chunk c (consumed by every wave before the barrier that opens the
   // iteration) with chunk c + kStages.
   static constexpr int kStages = kStages_;
-  static constexpr int kLdsBytes = kStages * kStageBytes;
-  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + kSDmaA + kSDmaB;
+  static constexpr int kSuperBase = kStages * kStageBytes;
+  static constexpr int kLdsBytes = kSuperBase + (kSuper ? 2 * kSuperBytes : 0);
+  // DMA loads per chunk and wave (without the super-stage loads).
+  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + (kSuper ? 0 : kSDmaA + kSDmaB);
+  static constexpr int kSuperLoads = 2;          // per 4 chunks: one A pair, one W pair
+  static_assert(!kSuper || (kAPerWave == 2 && kBPerWave == 2 && kStages == 4), "super-stage layout");
   static constexpr int kGroupM = 4;
   static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
   static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
   static constexpr int kLdsReads = 2 * (FM + FN);             // LDS reads per chunk and wave
   static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
   static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c + 1 landed
+  // With super-stages: at chunk c the loads issued after everything chunk
+  // c + 1 needs are those of chunks c - 2 and c - 1, plus the super-stage
+  // loads issued with chunk c - 2 or c - 1 when that is a multiple of 4.
+  static constexpr int kWaitSuper0 = lds::vmcnt_imm(2 * kLoadsPerWave);                // c % 4 in {0, 3}
+  static constexpr int kWaitSuper1 = lds::vmcnt_imm(2 * kLoadsPerWave + kSuperLoads);  // c % 4 in {1, 2}
   static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerWave < 64, "ring depth");
   static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
   static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
@@ -281,6 +297,8 @@ struct LdsCfg {
 // 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
 // of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
 typedef LdsCfg<2, 2, 4, 4, 1, 6, 4> LdsSquare;
+// The same with scale super-stages (K % 256 == 0).
+typedef LdsCfg<2, 2, 4, 4, 1, 6, 4, true> LdsSquareSuper;
 // 256 x 128 workgroups of 2 x 2 waves with 4 x 2 fragments, two per CU: the
 // tail of a launch whose last round of square tiles would be at most half
 // full (see launch_gemm).
@@ -346,14 +364,38 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
     const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
 #pragma unroll
     for (int i = 0; i < kAPerWave; ++i) dma16(ra, st + kA + (fa0 + i) * 1024, a_off[i], kq * 32u);
+    if constexpr (!C::kSuper) {
 #pragma unroll
-    for (int j = 0; j < C::kSDmaA; ++j)
-      dma4(rs, st + kSA + (fa0 + (C::kPairA ? 2 * j : j)) * C::kSFA, as_off[j], kq * 4u);
+      for (int j = 0; j < C::kSDmaA; ++j)
+        dma4(rs, st + kSA + (fa0 + (C::kPairA ? 2 * j : j)) * C::kSFA, as_off[j], kq * 4u);
+    }
 #pragma unroll
     for (int i = 0; i < kBPerWave; ++i) dma16(rb, st + kB + (fb0 + i) * 1024, b_off[i], kq * 1024u);
+    if constexpr (!C::kSuper) {
 #pragma unroll
-    for (int j = 0; j < C::kSDmaB; ++j)
-      dma4(rbs, st + kSB + (fb0 + (C::kPairB ? 2 * j : j)) * C::kSFB, bs_off[j], kq * 128u);
+      for (int j = 0; j < C::kSDmaB; ++j)
+        dma4(rbs, st + kSB + (fb0 + (C::kPairB ? 2 * j : j)) * C::kSFB, bs_off[j], kq * 128u);
+    }
+  };
+  // Super-stage sg (the scales of chunks 4 sg .. 4 sg + 3) into buffer
+  // sg % 2: lane (h, r) loads row r of the wave's A fragment fa0 + h (16
+  // bytes: 4 chunks of one row) and 16 bytes (rows 4 (r % 8) .., chunk r / 8)
+  // of the 512-byte group of weight tile fb0 + h.  Groups past the end of K
+  // re-load the last one.
+  const uint32_t a_sup_off = [&]() {
+    const uint32_t row = tm * BM + (fa0 + h) * 32 + r;
+    return row < p.M ? row * (p.K >> 4) : kOOB;
+  }();
+  const uint32_t b_sup_off = [&]() {
+    const uint32_t nt = nt0 + fb0 + h;
+    return nt < p.w_tiles ? nt * p.w_kc * 128u + r * 16u : kOOB;
+  }();
+  auto issue_super = [&](uint32_t sg) {
+    uint8_t* sb = smem + C::kSuperBase + (sg & 1u) * C::kSuperBytes;
+    const uint32_t last = (p.chunks >> 2) - 1;
+    const uint32_t sq = sg < last ? sg : last;
+    dma16(rs, sb + fa0 * 512, a_sup_off, sq * 16u);
+    dma16(rbs, sb + C::kSuperB + fb0 * 512, b_sup_off, sq * 512u);
   };
 
   struct Regs {
@@ -364,15 +406,23 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   // of the chunk).
   auto read_stage = [&](Regs& R, uint32_t kc) {
     const uint8_t* st = smem + (kc % kStages) * kStageBytes;
+    const uint8_t* sb = smem + C::kSuperBase + ((kc >> 2) & 1u) * C::kSuperBytes;
+    const uint32_t j = kc & 3u;
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
-      R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * C::kSFA + r * 4 + h * 2);
+      if constexpr (C::kSuper)
+        R.sa[f] = *(const uint16_t*)(sb + (wm * FM + f) * 512 + r * 16 + j * 4 + h * 2);
+      else
+        R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * C::kSFA + r * 4 + h * 2);
     }
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
-      R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * C::kSFB + r * 4 + h * 2);
+      if constexpr (C::kSuper)
+        R.sb[f] = *(const uint16_t*)(sb + C::kSuperB + (wn * FN + f) * 512 + j * 128 + r * 4 + h * 2);
+      else
+        R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * C::kSFB + r * 4 + h * 2);
     }
   };
 
@@ -406,14 +456,22 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
                                                       : __builtin_shufflevector(sB[f], sB[f], 0, 0));
   };
   // One chunk: wait until chunk c + 1 has landed, barrier, DMA of chunk
-  // c + kStages into the stage of chunk c, LDS reads of chunk c + 1 into
-  // `next`, decode + MFMA of `cur`.
-  auto step = [&](uint32_t c, const Regs& cur, Regs& next) {
+  // c + kStages into the stage of chunk c (and, with super-stages, at
+  // c % 4 == 0 the scales of chunks c + 4 .. c + 7 into the buffer that held
+  // those of chunks c - 4 .. c - 1), LDS reads of chunk c + 1 into `next`,
+  // decode + MFMA of `cur`.  pos_tag: c % 4 (super-stages) or 0.
+  auto step = [&](uint32_t c, const Regs& cur, Regs& next, auto pos_tag) {
+    constexpr int kPos = decltype(pos_tag)::value;
+    constexpr bool kIssueSuper = C::kSuper && kPos == 0;
     // Every LDS read of the previous iteration has been consumed by its
     // decode, so after the barrier the stage of chunk c may be refilled.
-    __builtin_amdgcn_s_waitcnt(C::kWaitNext);
+    if constexpr (C::kSuper)
+      __builtin_amdgcn_s_waitcnt(kPos == 1 || kPos == 2 ? C::kWaitSuper1 : C::kWaitSuper0);
+    else
+      __builtin_amdgcn_s_waitcnt(C::kWaitNext);
     __builtin_amdgcn_s_barrier();
     issue(c + kStages);
+    if constexpr (kIssueSuper) issue_super((c >> 2) + 1);
     read_stage(next, c + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -432,19 +490,28 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
     }
     // LDS reads spread over the first half of the chunk, DMA issues over the
     // first three quarters.
+    constexpr int kDma = C::kLoadsPerWave + (kIssueSuper ? C::kSuperLoads : 0);
     constexpr int kLdsEvery = (C::kMfma / 2) / C::kLdsReads;
-    constexpr int kDmaEvery = (3 * C::kMfma / 4) / C::kLoadsPerWave;
+    constexpr int kDmaEvery = (3 * C::kMfma / 4) / kDma;
 #pragma unroll
     for (int i = 0; i < C::kMfma; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
       if (i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                     // LDS read
-      if (i % kDmaEvery == 0 && i / kDmaEvery < C::kLoadsPerWave)
+      if (i % kDmaEvery == 0 && i / kDmaEvery < kDma)
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
     }
   };
+  using Pos0 = std::integral_constant<int, 0>;
+  using Pos1 = std::integral_constant<int, 1>;
+  using Pos2 = std::integral_constant<int, 2>;
+  using Pos3 = std::integral_constant<int, 3>;
 
+  if constexpr (C::kSuper) {
+    issue_super(0);                          // before chunk 0's codes: landed with them
+    __builtin_amdgcn_sched_barrier(0);       // keep that order (the waits count loads in issue order)
+  }
 #pragma unroll
   for (int s = 0; s < kStages; ++s) issue(s);
   __builtin_amdgcn_s_waitcnt(C::kWaitFirst);
@@ -453,9 +520,19 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   read_stage(cur, 0);
   scales(cur);
   decode_step(cur, 0, 0);
-  for (uint32_t c = 0; c < p.chunks; ++c) {
-    step(c, cur, nxt);
-    cur = nxt;
+  if constexpr (C::kSuper) {
+    // p.chunks % 4 == 0 (K % 256 == 0).
+    for (uint32_t c = 0; c < p.chunks; c += 4) {
+      step(c, cur, nxt, Pos0{});
+      step(c + 1, nxt, cur, Pos1{});
+      step(c + 2, cur, nxt, Pos2{});
+      step(c + 3, nxt, cur, Pos3{});
+    }
+  } else {
+    for (uint32_t c = 0; c < p.chunks; ++c) {
+      step(c, cur, nxt, Pos0{});
+      cur = nxt;
+    }
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
   __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -1112,13 +1189,17 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     const uint32_t tiles_m = (uint32_t)((M + LdsSquare::BM - 1) / LdsSquare::BM);
     const uint32_t tiles_n = (uint32_t)((N + LdsSquare::BN - 1) / LdsSquare::BN);
     const uint32_t n_cu = cu_count();
+    const bool super = (K % 256) == 0;   // scale super-stages: 16-byte aligned, whole groups of 4 chunks
     const uint32_t rem = n_cu ? (tiles_m * tiles_n) % n_cu : 0;
     if (rem != 0 && rem <= n_cu / 2 && rem % tiles_m == 0 && rem / tiles_m < tiles_n) {
       const uint32_t n_split = (tiles_n - rem / tiles_m) * LdsSquare::BN;
-      hipError_t e = launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, n_split, out_f32, stream);
+      hipError_t e = super ? launch_lds<LdsSquareSuper>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, n_split, out_f32, stream)
+                           : launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, n_split, out_f32, stream);
       if (e != hipSuccess) return e;
       return launch_lds<LdsTall>(a_codes, a_scales, a_g, wp, w_g, y, p, n_split, (uint32_t)N, out_f32, stream);
     }
+    if (super)
+      return launch_lds<LdsSquareSuper>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, (uint32_t)N, out_f32, stream);
     return launch_lds<LdsSquare>(a_codes, a_scales, a_g, wp, w_g, y, p, 0, (uint32_t)N, out_f32, stream);
   }
   return launch_reg<2, 2, 4, 4>(a_codes, a_scales, a_g, wp, w_g, y, p, out_f32, aligned, stream);
