@@ -298,7 +298,7 @@ struct LdsCfg {
 // of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
 typedef LdsCfg<2, 2, 4, 4, 1, 6, 4> LdsSquare;
 // The same with scale super-stages (K % 256 == 0).
-typedef LdsCfg<2, 2, 4, 4, 1, 6, 4, true> LdsSquareSuper;
+typedef LdsCfg<2, 2, 4, 4, 1, 5, 4, true> LdsSquareSuper;
 // 256 x 128 workgroups of 2 x 2 waves with 4 x 2 fragments, two per CU: the
 // tail of a launch whose last round of square tiles would be at most half
 // full (see launch_gemm).
