@@ -664,19 +664,37 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_reg_kernel(const uint8_t* _
 // while it decodes and multiplies the current one, and the partial sums meet
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
-// Split-K epilogue: the KS waves' partial sums of each fragment meet in LDS
-// (part: KS x 64 floatx16) and are summed in wave order (deterministic).
-// Plain outputs: fragment f is summed and stored by wave f % KS.  With the
-// GDN gate transform (kGate), whose transcendentals dominate the epilogue,
-// every wave takes 16 / KS of each lane's 16 accumulator entries of every
-// fragment instead, so that all waves share that arithmetic.  Each value is
-// scaled by its column's segment scale.
-template <int KS, int FM, int FN, bool kF32Out, bool kGate>
+// 1 / (G_A G_W[s]) for the column of lane r in each of the FN fragment
+// columns of a tile (0 when either scale is 0).  Taken before the main loop,
+// so that the loads of the scales are off the epilogue's path.
+template <int FN>
+__device__ __forceinline__ void segment_alpha(const GemmParams& p, float ga, const float* __restrict__ w_g,
+                                              uint32_t n0, uint32_t r, float (&alpha)[FN]) {
+#pragma unroll
+  for (int fb = 0; fb < FN; ++fb) {
+    const uint32_t col = n0 + fb * 32 + r;
+    int s = 0;
+#pragma unroll
+    for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+    const float prod = ga * w_g[s];
+    alpha[fb] = prod == 0.0f ? 0.0f : 1.0f / prod;
+  }
+}
+
+// Split-K epilogue: the KS waves' partial sums meet in LDS, kGroup fragments
+// at a time (part: kGroup x KS x 64 floatx16), and are summed in wave order
+// (deterministic).  Plain outputs: fragment f is summed and stored by wave
+// f % KS.  With the GDN gate transform (kGate), whose transcendentals
+// dominate the epilogue, every wave takes 16 / KS of each lane's 16
+// accumulator entries of every fragment instead, so that all waves share
+// that arithmetic.  Each value is scaled by its column's alpha.  LDS at part
+// must be free (a caller that used it for other data synchronizes first).
+template <int KS, int FM, int FN, int kGroup, bool kF32Out, bool kGate>
 __device__ __forceinline__ void splitk_epilogue(const floatx16 (&acc)[FM][FN], floatx16* part, const GemmParams& p,
-                                                float ga, const float* __restrict__ w_g, void* __restrict__ y,
+                                                const float (&alpha)[FN], void* __restrict__ y,
                                                 uint32_t m0, uint32_t n0, uint32_t wave, uint32_t lane) {
   static_assert(16 % KS == 0, "entries per wave");
-  constexpr int kPer = 16 / KS;
+  constexpr int kPer = 16 / KS, kFrags = FM * FN;
   const uint32_t r = lane & 31, h = lane >> 5;
   const float* partf = reinterpret_cast<const float*>(part);
   auto store = [&](float v, uint32_t row, uint32_t col) {
@@ -689,34 +707,36 @@ __device__ __forceinline__ void splitk_epilogue(const floatx16 (&acc)[FM][FN], f
     }
   };
 #pragma unroll
-  for (int fa = 0; fa < FM; ++fa) {
+  for (int g0 = 0; g0 < kFrags; g0 += kGroup) {
+    if (g0 > 0) __syncthreads();                   // the previous group has been read
 #pragma unroll
-    for (int fb = 0; fb < FN; ++fb) {
-      part[wave * 64 + lane] = acc[fa][fb];
-      __syncthreads();
+    for (int j = 0; j < kGroup; ++j)
+      if (g0 + j < kFrags) part[(j * KS + wave) * 64 + lane] = acc[(g0 + j) / FN][(g0 + j) % FN];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const int f = g0 + j;
+      if (f >= kFrags) break;
+      const int fa = f / FN, fb = f % FN;
       const uint32_t col = n0 + fb * 32 + r;
-      int s = 0;
-#pragma unroll
-      for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
-      const float prod = ga * w_g[s];
-      const float alpha = prod == 0.0f ? 0.0f : 1.0f / prod;
+      const floatx16* pj = part + j * KS * 64;
       if (kGate) {
+        const float* pf = partf + j * KS * 64 * 16;
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
           const uint32_t i = wave * kPer + e;               // accumulator entry of this wave
-          float sum = partf[lane * 16 + i];
+          float sum = pf[lane * 16 + i];
 #pragma unroll
-          for (int w = 1; w < KS; ++w) sum += partf[(w * 64 + lane) * 16 + i];
-          store(sum * alpha, m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
+          for (int w = 1; w < KS; ++w) sum += pf[(w * 64 + lane) * 16 + i];
+          store(sum * alpha[fb], m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
         }
-      } else if (wave == (uint32_t)((fa * FN + fb) % KS)) {
-        floatx16 sum = part[lane];
+      } else if (wave == (uint32_t)(f % KS)) {
+        floatx16 sum = pj[lane];
 #pragma unroll
-        for (int w = 1; w < KS; ++w) sum += part[w * 64 + lane];
+        for (int w = 1; w < KS; ++w) sum += pj[w * 64 + lane];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) store(sum[i] * alpha, m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
+        for (int i = 0; i < 16; ++i) store(sum[i] * alpha[fb], m0 + fa * 32 + (i >> 2) * 8 + h * 4 + (i & 3), col);
       }
-      __syncthreads();
     }
   }
 }
@@ -746,8 +766,8 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   constexpr int kScaleA = L::kScaleA, kScaleB = L::kScaleB, kStageBytes = L::kBytes;
   constexpr int kLoads = L::kLoads;                          // DMA loads per chunk and wave
   constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoads);
-  constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoads);
-  static_assert(kStages >= 2 && (kStages - 1) * kLoads < 64, "memory counter range");
+  constexpr int kWaitNext = lds::vmcnt_imm((kStages - 1) * kLoads);
+  static_assert(kStages >= 2 && kStages <= 4 && (kStages - 1) * kLoads < 64, "ring depth, memory counter range");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // The wave index is uniform: taking it through readfirstlane keeps the
   // chunk index, buffer descriptors and LDS addresses in scalar registers.
@@ -785,14 +805,16 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
   const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+  float alpha[FN];
+  segment_alpha<FN>(p, *a_g, w_g, n0, r, alpha);
 
   const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
   const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
   const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
   const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales, w_scale_bytes);
-  // DMA of this wave's i-th chunk into stage i % kStages.  Chunks past the
-  // end of K are never read; they re-load the last chunk so that every
-  // address stays inside its tensor.
+  // DMA of this wave's i-th chunk into stage i % kStages.  (Prologue loads
+  // of chunks past the end of K, when K is short, re-load the last chunk so
+  // that every address stays inside its tensor; they are never read.)
   auto issue = [&](uint32_t i) {
     const uint32_t kc = wave + KS * i;
     const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
@@ -826,10 +848,24 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
 #pragma unroll
     for (int fb = 0; fb < FN; ++fb) acc[fa][fb] = floatx16{};
 
+  // cur's stage is free once cur is in registers, so it is refilled before
+  // the wait for chunk i + 1: kStages - 1 chunks stay in flight through it.
+  // Near the end nothing is refilled, and the wait for chunk i + 1 lets
+  // exactly the chunks after it stay in flight (loads land in order).
   auto step = [&](uint32_t i, const Regs& cur, Regs& next) {
     __builtin_amdgcn_s_waitcnt(lds::kWaitLgkm0);       // cur read from its stage
-    __builtin_amdgcn_s_waitcnt(kWaitNext);              // chunk i + 1 landed
-    issue(i + kStages);                                 // refills cur's stage
+    if (i + kStages < n_mine) {
+      issue(i + kStages);                               // refills cur's stage
+      __builtin_amdgcn_s_waitcnt(kWaitNext);            // chunk i + 1 landed
+    } else {
+      const int rem = (int)n_mine - 2 - (int)i;         // chunks after i + 1 (< kStages - 1)
+      if (rem >= 2)
+        __builtin_amdgcn_s_waitcnt(lds::vmcnt_imm(2 * kLoads));
+      else if (rem == 1)
+        __builtin_amdgcn_s_waitcnt(lds::vmcnt_imm(kLoads));
+      else
+        __builtin_amdgcn_s_waitcnt(lds::vmcnt_imm(0));
+    }
     read_stage(next, i + 1);
     half2v sc[kFrags];
 #pragma unroll
@@ -873,12 +909,16 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
     step(i, cur, nxt);
     cur = nxt;
   }
-  // Drain this wave's DMA (chunks past the end) before the ring is reused.
+  // Drain this wave's DMA (prologue loads past a short K) before the ring
+  // is reused for the partial sums.
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
 
-  splitk_epilogue<KS, FM, FN, kF32Out, kGate>(acc, reinterpret_cast<floatx16*>(smem), p, *a_g, w_g, y, m0, n0,
-                                              wave, lane);
+  constexpr int kFit = (kStages * kStageBytes) / (64 * 64);   // fragments whose partials fit the ring
+  constexpr int kGroup = kFit < FM * FN ? kFit : FM * FN;
+  static_assert(kGroup >= 1, "partial sums of one fragment fit the ring");
+  splitk_epilogue<KS, FM, FN, kGroup, kF32Out, kGate>(acc, reinterpret_cast<floatx16*>(smem), p, alpha, y, m0, n0,
+                                                      wave, lane);
 }
 
 // ------------------------------------------- fused quantize + tall-skinny GEMM
@@ -959,6 +999,8 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
   const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
   const __amdgpu_buffer_rsrc_t rbs = rsrc(w_packed + p.w_scale_offset, p.w_bytes - p.w_scale_offset);
   const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+  float alpha[FN];
+  segment_alpha<FN>(p, g, w_g, n0, r, alpha);
 
   struct Chunk {
     int4v x[FM][4];         // per fragment, the lane's 32 bf16 values
@@ -1050,7 +1092,7 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
     run(std::integral_constant<bool, true>{});
   else
     run(std::integral_constant<bool, false>{});
-  splitk_epilogue<KS, FM, FN, kF32Out, false>(acc, part, p, g, w_g, y, m0, n0, wave, lane);
+  splitk_epilogue<KS, FM, FN, 1, kF32Out, false>(acc, part, p, alpha, y, m0, n0, wave, lane);
 }
 
 template <int KS, int FM, int FN, int kDepth>
