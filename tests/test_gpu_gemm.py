@@ -80,6 +80,9 @@ def test_gemm_tiny_workload():
     (1, 300, 1040, [0, 300]),              # small-M, one row, K % 64 != 0
     (17, 4100, 128, [0, 4000, 4100]),      # small-M, many column tiles, 2 chunks < 8 waves
     (777, 1300, 384, [0, 500, 1300]),      # prefill path: 4 x 6 tiles of 256 x 256, ragged M and N
+    (40, 96, 768, [0, 48, 96]),            # tall-skinny split-K: 3 chunks per wave (= ring stages)
+    (5, 200, 1024, [0, 100, 200]),         # small-M split-K: 4 chunks per wave (one refill)
+    (9, 64, 960, [0, 64]),                 # split-K: 15 chunks, 4/4/4/3 per wave
 ])
 def test_gemm_ragged_shapes(m, n, k, offs):
     rng = np.random.default_rng(m * 7 + n * 3 + k)
