@@ -115,7 +115,7 @@ def main():
                     help="copy a 1 GiB buffer 3 times with a plain device copy (for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build runs the NVFP4 linear layer on a single "
+        print("bench.py measures one GPU only: the library runs the NVFP4 linear layer on a single "
               "MI355X (no multi-GPU path); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
