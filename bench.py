@@ -104,12 +104,86 @@ def cpu_baseline(cfg, x_bits, w_bits, rows=8192, cols_per_seg=17408):
     }
 
 
+def measure_workload(name, steps, warmup, dev, log_fn):
+    """GEMM and dynamic act-quant of one more workload, timed like the
+    headline step (HIP events on the launch stream around each launch);
+    not part of `value`."""
+    import numpy as np
+    import torch
+    from paper_2609_04098_amd import linear as L
+    from paper_2609_04098_amd import nvfp4 as C
+    from paper_2609_04098_amd import synth
+
+    cfg = synth.CONFIGS[name]
+    log_fn("drawing inputs for %s" % cfg.description)
+    to_dev = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(dev)
+    x = to_dev(synth.make_x(cfg))
+    pw = L.pack_weight(to_dev(synth.make_w(cfg)), cfg.seg_offsets)
+    aq = L.alloc_act(cfg.m, cfg.k, dev)
+    ws = L.act_workspace(cfg.m, cfg.k, dev)
+    y = torch.empty((cfg.m, cfg.n), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        L.quantize_act(x, out=aq, workspace=ws)
+        L.gemm(aq, pw, out=y)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record(stream)
+        L.quantize_act(x, out=aq, workspace=ws)
+        ev[i][1].record(stream)
+        L.gemm(aq, pw, out=y)
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    aq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    aq_bytes = cfg.m * cfg.k * (2 + 0.5 + 1.0 / 16)
+    gemm_bytes = (cfg.m + cfg.n) * cfg.k * (0.5 + 1.0 / 16) + 2.0 * cfg.m * cfg.n
+    out = {
+        "M": cfg.m, "N": cfg.n, "K": cfg.k, "segments": list(cfg.segments),
+        "gemm_kernels": L.gemm_kernels(cfg.m, cfg.n, cfg.k),
+        "gemm_avg_ms": round(gemm_ms, 4),
+        "gemm_tflops": round(cfg.flops / (gemm_ms * 1e-3) / 1e12, 2),
+        "gemm_frac_mfma_f16": round(cfg.flops / (gemm_ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+        "gemm_frac_hbm": round(gemm_bytes / (gemm_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "act_quant_avg_ms": round(aq_ms, 4),
+        "act_quant_gbs": round(aq_bytes / (aq_ms * 1e-3) / 1e9, 1),
+        "act_quant_frac_hbm": round(aq_bytes / (aq_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "tflops_incl_act_quant": round(cfg.flops / ((aq_ms + gemm_ms) * 1e-3) / 1e12, 2),
+    }
+    if cfg.n <= 128 and cfg.k % 64 == 0:
+        # Narrow output: act-quant fused into the GEMM, calibrated G (one pass
+        # over X) and dynamic G (amax pass + one fused launch).
+        g_static = aq.g.clone()
+        gf = torch.empty(1, dtype=torch.float32, device=dev)
+        for mode_name, mode in (("dynamic", C.NVFP4_DYNAMIC), ("static", C.NVFP4_STATIC)):
+            gb = gf if mode == C.NVFP4_DYNAMIC else g_static
+            wsp = ws if mode == C.NVFP4_DYNAMIC else None
+            call = lambda: C.nvfp4_quantize_gemm(x, gb, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, mode, wsp,
+                                                 stream=stream)
+            for _ in range(warmup):
+                call()
+            fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+            for i in range(steps):
+                fev[i][0].record(stream)
+                call()
+                fev[i][1].record(stream)
+            torch.cuda.synchronize()
+            f_ms = float(np.mean([a.elapsed_time(b) for a, b in fev]))
+            out["fused_quantize_gemm_%s_ms" % mode_name] = round(f_ms, 4)
+            out["fused_quantize_gemm_%s_tflops" % mode_name] = round(cfg.flops / (f_ms * 1e-3) / 1e12, 2)
+    del x, pw, aq, ws, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the secondary per-workload figures (gdn_qkv, mlp_down, ab_gates)")
     ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="copy a 1 GiB buffer 3 times with a plain device copy (for scaling HBM byte counters)")
@@ -289,8 +363,7 @@ def main():
         "pct_of_mfma_peak": round(100.0 * value / MFMA_F16_PEAK_TFLOPS, 2),
         "roofline": {
             "bound": "mfma",
-            "kernel": ("gemm_splitk_kernel<4, 2, 3> (tall-skinny NVFP4 GEMM + segment-scaled bf16 epilogue)"
-                       if cfg.n <= 96 else "gemm_lds_kernel<LdsSquare, false> (256 x 256 NVFP4 GEMM + segment-scaled bf16 epilogue)"),
+            "kernel": " + ".join(L.gemm_kernels(cfg.m, cfg.n, cfg.k)) + ", bf16 out",
             "achieved": round(gemm_tflops, 2),
             "peak": MFMA_F16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
@@ -322,6 +395,11 @@ def main():
         "prepack_ms": round(prepack_ms, 3),
         "gemm_source_sha256_16": gemm_source_hash(),
     }
+    if not args.no_other_workloads and args.workload == WORKLOAD:
+        result["other_workloads"] = {}
+        for name in ("gdn_qkv", "mlp_down", "ab_gates"):
+            result["other_workloads"][name] = measure_workload(name, max(5, args.steps // 2), max(2, args.warmup), dev,
+                                                               log)
     if not args.no_cpu_baseline:
         log("CPU oracle baseline on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(cfg, x_bits, w_bits)

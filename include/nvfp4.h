@@ -64,15 +64,15 @@ enum nvfp4_scale_mode {
 
 /* Output element type of nvfp4_gemm. */
 enum nvfp4_out_dtype {
-  NVFP4_OUT_BF16 = 0,      /* round-to-nearest-even of the FP32 result */
-  NVFP4_OUT_F32 = 1
+  NVFP4_BF16 = 0,      /* round-to-nearest-even of the FP32 result */
+  NVFP4_F32 = 1
 };
 
 #define NVFP4_BLOCK 16          /* elements per block scale, along K */
 #define NVFP4_MAX_SEGMENTS 8    /* fused segments per GEMM */
 
 /* Human-readable name of a status code (static string, never NULL). */
-const char* nvfp4_status_string(int status);
+const char* nvfp4_status_str(int status);
 
 /* The hipError_t value of the last NVFP4_EHIP failure on the calling host
  * thread (0 if none). */
@@ -81,7 +81,7 @@ int nvfp4_last_hip_error(void);
 /* Workspace bytes nvfp4_quantize_act needs for an M x K activation (the
  * per-workgroup partial maxima of the dynamic global scale); 0 is a valid
  * answer only in static mode, and the dynamic answer is returned here. */
-size_t nvfp4_quantize_act_workspace_bytes(int64_t M, int64_t K);
+size_t nvfp4_quantize_act_workspace(int64_t M, int64_t K);
 
 /*
  * Dynamic activation quantization (paper, section 2: NVFP4; section 9
@@ -93,7 +93,7 @@ size_t nvfp4_quantize_act_workspace_bytes(int64_t M, int64_t K);
  *   g_enc    one device float: written with G in NVFP4_DYNAMIC mode, read in
  *            NVFP4_STATIC mode (must then be finite and >= 0).
  *   workspace, workspace_bytes: device scratch of at least
- *            nvfp4_quantize_act_workspace_bytes(M, K) bytes in dynamic mode;
+ *            nvfp4_quantize_act_workspace(M, K) bytes in dynamic mode;
  *            unused in static mode (may be NULL).  Its contents on entry do
  *            not matter; calls sharing one workspace must be ordered.
  * Requirements: M >= 0, K >= 0, K % 16 == 0, M * K < 2^31.
@@ -132,7 +132,7 @@ int nvfp4_rmsnorm_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                                uint8_t* scales, const float* g_enc, void* y,
                                int64_t ldy, void* stream);
 
-/* Bytes of the packed weight buffer for an N x K weight:/* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
+/* Bytes of the packed weight buffer for an N x K weight: the GEMM-private
  * tile layout of the codes and block scales, N padded to 32 and K to 64. */
 size_t nvfp4_packed_weight_bytes(int64_t N, int64_t K);
 
@@ -219,6 +219,17 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                const void* w_packed, int64_t N,
                const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg,
                void* y, int64_t ldy, int y_dtype, void* stream);
+
+/*
+ * Which kernels nvfp4_gemm launches for an M x N x K call on the current
+ * device (diagnostics: benchmarks and profiles name the kernel they time).
+ * part 0: the first launch; part 1: the second launch of a shape whose last
+ * round of tiles runs as narrower tiles.  Returns a static string naming the
+ * kernel and its tile shape, or NULL when that launch does not exist (M == 0,
+ * no second launch) or the arguments are invalid (K % 16 != 0, N < 1,
+ * M < 0, part not 0 or 1) or the device cannot be queried.
+ */
+const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part);
 
 /*
  * The fused GDN gate projection with the gate transform in its epilogue

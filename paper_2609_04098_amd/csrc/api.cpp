@@ -62,7 +62,7 @@ bool valid_segments(const int64_t* offs, int n_seg, int64_t n) {
 
 extern "C" {
 
-const char* nvfp4_status_string(int status) {
+const char* nvfp4_status_str(int status) {
   switch (status) {
     case NVFP4_OK: return "NVFP4_OK";
     case NVFP4_EINVAL: return "NVFP4_EINVAL: invalid argument";
@@ -75,7 +75,7 @@ const char* nvfp4_status_string(int status) {
 
 int nvfp4_last_hip_error(void) { return g_last_hip_error; }
 
-size_t nvfp4_quantize_act_workspace_bytes(int64_t M, int64_t K) {
+size_t nvfp4_quantize_act_workspace(int64_t M, int64_t K) {
   (void)M;
   (void)K;
   return (size_t)nvfp4::kActPartials * sizeof(float);
@@ -97,7 +97,7 @@ int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t
   const bool dynamic = mode == NVFP4_DYNAMIC;
   if (dynamic && !empty) {
     if (workspace == nullptr || !aligned16(workspace)) return NVFP4_EINVAL;
-    if (workspace_bytes < nvfp4_quantize_act_workspace_bytes(M, K)) return NVFP4_EWORKSPACE;
+    if (workspace_bytes < nvfp4_quantize_act_workspace(M, K)) return NVFP4_EWORKSPACE;
   }
   int st = check_device();
   if (st != NVFP4_OK) return st;
@@ -200,7 +200,7 @@ int nvfp4_harmonize_weight(void* packed, int64_t N, int64_t K, const int64_t* se
 int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
                int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
                const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype, void* stream) {
-  if (y_dtype != NVFP4_OUT_BF16 && y_dtype != NVFP4_OUT_F32) return NVFP4_EINVAL;
+  if (y_dtype != NVFP4_BF16 && y_dtype != NVFP4_F32) return NVFP4_EINVAL;
   if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
   if (ldy < N) return NVFP4_EINVAL;
   if (M * K >= kI32Lim || N * K >= kI32Lim || M * ldy >= kI32Lim) return NVFP4_EINVAL;
@@ -213,22 +213,28 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g
   if (M > 0) {
     if (a_codes == nullptr || a_scales == nullptr || y == nullptr) return NVFP4_EINVAL;
     if (!aligned16(a_codes) || !aligned16(a_scales)) return NVFP4_EINVAL;
-    const uintptr_t elem = y_dtype == NVFP4_OUT_F32 ? 4u : 2u;
+    const uintptr_t elem = y_dtype == NVFP4_F32 ? 4u : 2u;
     if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
   }
   int st = check_device();
   if (st != NVFP4_OK) return st;
   hipError_t e = nvfp4::launch_gemm(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg,
-                                    w_g_enc_seg, y, ldy, y_dtype == NVFP4_OUT_F32,
+                                    w_g_enc_seg, y, ldy, y_dtype == NVFP4_F32,
                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
+const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part) {
+  if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0 || (part != 0 && part != 1)) return nullptr;
+  if (check_device() != NVFP4_OK) return nullptr;
+  return nvfp4::gemm_kernel_for(M, N, K, part);
 }
 
 int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
                          int64_t K, const void* w_packed, int64_t H, const float* w_g_enc_seg,
                          const float* a_log, const float* dt_bias, void* y, int64_t ldy, int y_dtype,
                          void* stream) {
-  if (y_dtype != NVFP4_OUT_BF16 && y_dtype != NVFP4_OUT_F32) return NVFP4_EINVAL;
+  if (y_dtype != NVFP4_BF16 && y_dtype != NVFP4_F32) return NVFP4_EINVAL;
   if (M < 0 || H < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
   const int64_t N = 2 * H;
   if (ldy < N) return NVFP4_EINVAL;
@@ -244,14 +250,14 @@ int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const 
   if (M > 0) {
     if (a_codes == nullptr || a_scales == nullptr || y == nullptr) return NVFP4_EINVAL;
     if (!aligned16(a_codes) || !aligned16(a_scales)) return NVFP4_EINVAL;
-    const uintptr_t elem = y_dtype == NVFP4_OUT_F32 ? 4u : 2u;
+    const uintptr_t elem = y_dtype == NVFP4_F32 ? 4u : 2u;
     if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
   }
   if (K % 64 != 0) return NVFP4_EUNSUPPORTED;
   int st = check_device();
   if (st != NVFP4_OK) return st;
   hipError_t e = nvfp4::launch_gemm_gdn_gates(a_codes, a_scales, a_g_enc, M, K, w_packed, H, w_g_enc_seg, a_log,
-                                              dt_bias, y, ldy, y_dtype == NVFP4_OUT_F32,
+                                              dt_bias, y, ldy, y_dtype == NVFP4_F32,
                                               static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
@@ -261,7 +267,7 @@ int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float*
                         const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg, uint8_t* a_codes,
                         uint8_t* a_scales, void* y, int64_t ldy, int y_dtype, void* stream) {
   if (mode != NVFP4_DYNAMIC && mode != NVFP4_STATIC) return NVFP4_EINVAL;
-  if (y_dtype != NVFP4_OUT_BF16 && y_dtype != NVFP4_OUT_F32) return NVFP4_EINVAL;
+  if (y_dtype != NVFP4_BF16 && y_dtype != NVFP4_F32) return NVFP4_EINVAL;
   if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
   if (ldy < N) return NVFP4_EINVAL;
   if (M * K >= kI32Lim || N * K >= kI32Lim || M * ldy >= kI32Lim) return NVFP4_EINVAL;
@@ -277,19 +283,19 @@ int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float*
     if (ldx < K || ldx % 8 != 0 || M * ldx >= kI32Lim) return NVFP4_EINVAL;
     if (x == nullptr || y == nullptr || !aligned16(x)) return NVFP4_EINVAL;
     if (a_codes != nullptr && (!aligned16(a_codes) || !aligned16(a_scales))) return NVFP4_EINVAL;
-    const uintptr_t elem = y_dtype == NVFP4_OUT_F32 ? 4u : 2u;
+    const uintptr_t elem = y_dtype == NVFP4_F32 ? 4u : 2u;
     if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
   }
   if (dynamic) {
     if (workspace == nullptr || !aligned16(workspace)) return NVFP4_EINVAL;
-    if (workspace_bytes < nvfp4_quantize_act_workspace_bytes(M, K)) return NVFP4_EWORKSPACE;
+    if (workspace_bytes < nvfp4_quantize_act_workspace(M, K)) return NVFP4_EWORKSPACE;
   }
   if (N > 128 || K % 64 != 0) return NVFP4_EUNSUPPORTED;
   int st = check_device();
   if (st != NVFP4_OK) return st;
   hipError_t e = nvfp4::launch_quant_gemm(x, M, K, ldx, a_g_enc, dynamic, static_cast<float*>(workspace), w_packed,
                                           N, seg_offsets, n_seg, w_g_enc_seg, a_codes, a_scales, y, ldy,
-                                          y_dtype == NVFP4_OUT_F32, static_cast<hipStream_t>(stream));
+                                          y_dtype == NVFP4_F32, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 

@@ -1,0 +1,338 @@
+// The prefill GEMM kernel (gemm_lds_kernel) and its launcher template; each
+// launched configuration is instantiated in its own translation unit
+// (gemm_lds_square.hip, gemm_lds_tall.hip; the super-stage kernel, whose
+// schedule takes minutes to compile, one output type per unit:
+// gemm_lds_super.hip, gemm_lds_super_f32.hip).
+#pragma once
+
+#include "gemm_common.h"
+
+namespace nvfp4 {
+
+// Workgroup shape of the LDS kernel: WM x WN waves, each owning an
+// FM x FN block of 32 x 32 accumulator fragments; kOcc workgroups per CU.
+template <int WM_, int WN_, int FM_, int FN_, int kOcc_, int kValu_, int kStages_, bool kSuper_ = false>
+struct LdsCfg {
+  static constexpr int WM = WM_, WN = WN_, FM = FM_, FN = FN_, kOcc = kOcc_;
+  // kSuper (K % 256 == 0): the scales of 4 consecutive chunks move together,
+  // one 16-byte DMA per fragment pair (a row's 4 scale dwords are
+  // contiguous), into two alternating scale "super-stages" beside the ring.
+  static constexpr bool kSuper = kSuper_;
+  static constexpr int kWaves = WM * WN, kThreads = kWaves * 64;
+  static constexpr int BM = WM * FM * 32, BN = WN * FN * 32;
+  static constexpr int NFA = WM * FM, NFB = WN * FN;         // fragments per workgroup
+  // Each wave moves the same number of A and B fragments (codes + scales).
+  static constexpr int kAPerWave = NFA / kWaves, kBPerWave = NFB / kWaves;
+  // Scales: one dword of 4 block scales per fragment row and chunk.  With an
+  // even count per wave, one DMA moves the scales of two fragments (64
+  // distinct rows, 128 B per fragment slot); with an odd count, one DMA per
+  // fragment (both half-waves load the same 32 rows; 256 B slots).
+  static constexpr bool kPairA = kAPerWave % 2 == 0, kPairB = kBPerWave % 2 == 0;
+  static constexpr int kSFA = kPairA ? 128 : 256, kSFB = kPairB ? 128 : 256;
+  static constexpr int kSDmaA = kPairA ? kAPerWave / 2 : kAPerWave, kSDmaB = kPairB ? kBPerWave / 2 : kBPerWave;
+  // One stage of the ring: raw codes (1 KB per fragment), then the scale
+  // slots, of one 64-deep chunk.
+  static constexpr int kA = 0, kB = NFA * 1024, kSA = kB + NFB * 1024, kSB = kSA + NFA * kSFA;
+  static constexpr int kStageBytes = kSuper ? kSA : kSB + NFB * kSFB;
+  // A super-stage: per A fragment [32 rows][4 chunks][4 B] (512 B), then per
+  // W fragment [4 chunks][32 rows][4 B] (512 B, the packed order).
+  static constexpr int kSuperB = NFA * 512, kSuperBytes = kSuperB + NFB * 512;
+  // kStages 64-deep stages in the ring; iteration c refills the stage of
+  // chunk c (consumed by every wave before the barrier that opens the
+  // iteration) with chunk c + kStages.
+  static constexpr int kStages = kStages_;
+  static constexpr int kSuperBase = kStages * kStageBytes;
+  static constexpr int kLdsBytes = kSuperBase + (kSuper ? 2 * kSuperBytes : 0);
+  // DMA loads per chunk and wave (without the super-stage loads).
+  static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + (kSuper ? 0 : kSDmaA + kSDmaB);
+  static constexpr int kSuperLoads = 2;          // per 4 chunks: one A pair, one W pair
+  static_assert(!kSuper || (kAPerWave == 2 && kBPerWave == 2 && kStages == 4), "super-stage layout");
+  static constexpr int kGroupM = 4;
+  static constexpr int kMfma = 4 * FM * FN;                   // MFMAs per chunk and wave
+  static constexpr int kValuPerMfma = kValu_;                 // schedule: VALU slots after each MFMA
+  static constexpr int kLdsReads = 2 * (FM + FN);             // LDS reads per chunk and wave
+  static constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoadsPerWave);   // chunk 0 landed
+  static constexpr int kWaitNext = lds::vmcnt_imm((kStages - 2) * kLoadsPerWave);    // chunk c + 1 landed
+  // With super-stages: at chunk c the loads issued after everything chunk
+  // c + 1 needs are those of chunks c - 2 and c - 1, plus the super-stage
+  // loads issued with chunk c - 2 or c - 1 when that is a multiple of 4.
+  static constexpr int kWaitSuper0 = lds::vmcnt_imm(2 * kLoadsPerWave);                // c % 4 in {0, 3}
+  static constexpr int kWaitSuper1 = lds::vmcnt_imm(2 * kLoadsPerWave + kSuperLoads);  // c % 4 in {1, 2}
+  static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerWave < 64, "ring depth");
+  static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
+  static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
+  static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
+};
+
+// The launched shape: 256 x 256 workgroups of 2 x 2 waves, each wave a
+// 128 x 128 block (4 x 4 fragments, 256 accumulator registers), one
+// workgroup per CU.  Per chunk a wave decodes 8 fragments for 64 MFMAs
+// (4 VALU per MFMA); with 4 x 2 fragments and two waves per SIMD it was
+// 6 per MFMA and measured 4-10% slower on the prefill shapes, as did rings
+// of 3 or 6 stages.  Its own VALU co-issues with its MFMAs.
+typedef LdsCfg<2, 2, 4, 4, 1, 6, 4> LdsSquare;
+// The same with scale super-stages (K % 256 == 0).
+typedef LdsCfg<2, 2, 4, 4, 1, 5, 4, true> LdsSquareSuper;
+// 256 x 128 workgroups of 2 x 2 waves with 4 x 2 fragments, two per CU: the
+// tail of a launch whose last round of square tiles would be at most half
+// full (see launch_gemm).
+typedef LdsCfg<2, 2, 4, 2, 2, 5, 4> LdsTall;
+static_assert(LdsSquare::BM == kSquareTile && LdsSquare::BN == kSquareTile && LdsSquareSuper::BN == kSquareTile,
+              "square tile of the dispatch");
+
+template <class C, bool kF32Out>
+__global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
+                                                                   const uint8_t* __restrict__ a_scales,
+                                                                   const float* __restrict__ a_g,
+                                                                   const uint8_t* __restrict__ w_packed,
+                                                                   const float* __restrict__ w_g,
+                                                                   void* __restrict__ y, GemmParams p) {
+  constexpr int WN = C::WN, FM = C::FM, FN = C::FN, BM = C::BM, BN = C::BN;
+  constexpr int kA = C::kA, kB = C::kB, kSA = C::kSA, kSB = C::kSB, kStages = C::kStages;
+  constexpr int kStageBytes = C::kStageBytes, kAPerWave = C::kAPerWave, kBPerWave = C::kBPerWave;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const uint32_t lane = threadIdx.x & 63, wave = wave_index();
+  const uint32_t r = lane & 31, h = lane >> 5;
+  uint32_t tm, tn;
+  tile_of<C::kGroupM>(p, tm, tn);
+  const uint32_t wm = wave / WN, wn = wave % WN;
+
+  // Per-lane offsets are fixed; the chunk advances the descriptors' base
+  // (and shrinks their size) in scalar registers.  Rows >= M and tiles past
+  // the packed weight get offsets beyond every descriptor: zeros.
+  // Scale DMA j: lane (h, r) loads the scale dword of row r of fragment
+  // j * 2 + h of the wave's pair (paired), or of fragment j (single).
+  uint32_t a_off[kAPerWave], as_off[C::kSDmaA], b_off[kBPerWave], bs_off[C::kSDmaB];
+  const uint32_t fa0 = kAPerWave * wave, fb0 = kBPerWave * wave;   // first fragment this wave loads
+  const uint32_t nt0 = (p.n_off >> 5) + tn * (BN / 32);             // first weight tile of the tile
+#pragma unroll
+  for (int i = 0; i < kAPerWave; ++i) {
+    const uint32_t row = tm * BM + (fa0 + i) * 32 + r;
+    a_off[i] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < C::kSDmaA; ++j) {
+    const uint32_t row = tm * BM + (fa0 + (C::kPairA ? 2 * j + h : j)) * 32 + r;
+    as_off[j] = row < p.M ? row * (p.K >> 4) : kOOB;
+  }
+#pragma unroll
+  for (int i = 0; i < kBPerWave; ++i) {
+    const uint32_t nt = nt0 + fb0 + i;
+    b_off[i] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+  }
+#pragma unroll
+  for (int j = 0; j < C::kSDmaB; ++j) {
+    const uint32_t nt = nt0 + fb0 + (C::kPairB ? 2 * j + h : j);
+    bs_off[j] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u : kOOB;
+  }
+  const uint8_t* w_scales = w_packed + p.w_scale_offset;
+  const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
+
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales, w_scale_bytes);
+  // DMA of chunk kc into stage kc % kStages.  The ring runs kStages - 1
+  // chunks past the end of K; those stages are never read, and re-load the
+  // last chunk so that every address stays inside its tensor.
+  auto issue = [&](uint32_t kc) {
+    uint8_t* st = smem + (kc % kStages) * kStageBytes;
+    const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
+#pragma unroll
+    for (int i = 0; i < kAPerWave; ++i) dma16(ra, st + kA + (fa0 + i) * 1024, a_off[i], kq * 32u);
+    if constexpr (!C::kSuper) {
+#pragma unroll
+      for (int j = 0; j < C::kSDmaA; ++j)
+        dma4(rs, st + kSA + (fa0 + (C::kPairA ? 2 * j : j)) * C::kSFA, as_off[j], kq * 4u);
+    }
+#pragma unroll
+    for (int i = 0; i < kBPerWave; ++i) dma16(rb, st + kB + (fb0 + i) * 1024, b_off[i], kq * 1024u);
+    if constexpr (!C::kSuper) {
+#pragma unroll
+      for (int j = 0; j < C::kSDmaB; ++j)
+        dma4(rbs, st + kSB + (fb0 + (C::kPairB ? 2 * j : j)) * C::kSFB, bs_off[j], kq * 128u);
+    }
+  };
+  // Super-stage sg (the scales of chunks 4 sg .. 4 sg + 3) into buffer
+  // sg % 2: lane (h, r) loads row r of the wave's A fragment fa0 + h (16
+  // bytes: 4 chunks of one row) and 16 bytes (rows 4 (r % 8) .., chunk r / 8)
+  // of the 512-byte group of weight tile fb0 + h.  Groups past the end of K
+  // re-load the last one.
+  const uint32_t a_sup_off = [&]() {
+    const uint32_t row = tm * BM + (fa0 + h) * 32 + r;
+    return row < p.M ? row * (p.K >> 4) : kOOB;
+  }();
+  const uint32_t b_sup_off = [&]() {
+    const uint32_t nt = nt0 + fb0 + h;
+    return nt < p.w_tiles ? nt * p.w_kc * 128u + r * 16u : kOOB;
+  }();
+  auto issue_super = [&](uint32_t sg) {
+    uint8_t* sb = smem + C::kSuperBase + (sg & 1u) * C::kSuperBytes;
+    const uint32_t last = (p.chunks >> 2) - 1;
+    const uint32_t sq = sg < last ? sg : last;
+    dma16(rs, sb + fa0 * 512, a_sup_off, sq * 16u);
+    dma16(rbs, sb + C::kSuperB + fb0 * 512, b_sup_off, sq * 512u);
+  };
+
+  struct Regs {
+    int4v ca[FM], cb[FN];
+    uint32_t sa[FM], sb[FN];   // low 16 bits: the lane's two block scales
+  };
+  // Lane (h, r) takes the half h of row r's scale dword (blocks 2h, 2h + 1
+  // of the chunk).
+  auto read_stage = [&](Regs& R, uint32_t kc) {
+    const uint8_t* st = smem + (kc % kStages) * kStageBytes;
+    const uint8_t* sb = smem + C::kSuperBase + ((kc >> 2) & 1u) * C::kSuperBytes;
+    const uint32_t j = kc & 3u;
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      R.ca[f] = *(const int4v*)(st + kA + (wm * FM + f) * 1024 + lane * 16);
+      if constexpr (C::kSuper)
+        R.sa[f] = *(const uint16_t*)(sb + (wm * FM + f) * 512 + r * 16 + j * 4 + h * 2);
+      else
+        R.sa[f] = *(const uint16_t*)(st + kSA + (wm * FM + f) * C::kSFA + r * 4 + h * 2);
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      R.cb[f] = *(const int4v*)(st + kB + (wn * FN + f) * 1024 + lane * 16);
+      if constexpr (C::kSuper)
+        R.sb[f] = *(const uint16_t*)(sb + C::kSuperB + (wn * FN + f) * 512 + j * 128 + r * 4 + h * 2);
+      else
+        R.sb[f] = *(const uint16_t*)(st + kSB + (wn * FN + f) * C::kSFB + r * 4 + h * 2);
+    }
+  };
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx16{};
+
+  // The decode of MFMA step 0 of chunk c + 1 runs beside the MFMAs of step 3
+  // of chunk c, so no iteration starts with a run of VALU work in front of
+  // its first MFMA (one wave per SIMD: nothing else would cover it).
+  half2v sA[FM], sB[FN];
+  half8 av[2][FM], bv[2][FN];
+  auto scales = [&](const Regs& R) {
+#pragma unroll
+    for (int f = 0; f < FM; ++f) sA[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(R.sa[f], 1.0f, false);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) sB[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(R.sb[f], 1.0f, false);
+  };
+  // Decode MFMA step j (0..3) of R into buffer u; steps 0, 1 use the first
+  // block scale of the lane, steps 2, 3 the second.
+  auto decode_step = [&](const Regs& R, int j, int u) {
+#pragma unroll
+    for (int f = 0; f < FM; ++f)
+      av[u][f] = decode8((uint32_t)R.ca[f][j], j >> 1 ? __builtin_shufflevector(sA[f], sA[f], 1, 1)
+                                                      : __builtin_shufflevector(sA[f], sA[f], 0, 0));
+#pragma unroll
+    for (int f = 0; f < FN; ++f)
+      bv[u][f] = decode8((uint32_t)R.cb[f][j], j >> 1 ? __builtin_shufflevector(sB[f], sB[f], 1, 1)
+                                                      : __builtin_shufflevector(sB[f], sB[f], 0, 0));
+  };
+  // One chunk: wait until chunk c + 1 has landed, barrier, DMA of chunk
+  // c + kStages into the stage of chunk c (and, with super-stages, at
+  // c % 4 == 0 the scales of chunks c + 4 .. c + 7 into the buffer that held
+  // those of chunks c - 4 .. c - 1), LDS reads of chunk c + 1 into `next`,
+  // decode + MFMA of `cur`.  pos_tag: c % 4 (super-stages) or 0.
+  auto step = [&](uint32_t c, const Regs& cur, Regs& next, auto pos_tag) {
+    constexpr int kPos = decltype(pos_tag)::value;
+    constexpr bool kIssueSuper = C::kSuper && kPos == 0;
+    // Every LDS read of the previous iteration has been consumed by its
+    // decode, so after the barrier the stage of chunk c may be refilled.
+    if constexpr (C::kSuper)
+      __builtin_amdgcn_s_waitcnt(kPos == 1 || kPos == 2 ? C::kWaitSuper1 : C::kWaitSuper0);
+    else
+      __builtin_amdgcn_s_waitcnt(C::kWaitNext);
+    __builtin_amdgcn_s_barrier();
+    issue(c + kStages);
+    if constexpr (kIssueSuper) issue_super((c >> 2) + 1);
+    read_stage(next, c + 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = j & 1;
+      if (j < 3) {
+        decode_step(cur, j + 1, u ^ 1);
+      } else {
+        scales(next);
+        decode_step(next, 0, 0);
+      }
+#pragma unroll
+      for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+        for (int fb = 0; fb < FN; ++fb)
+          acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
+    }
+    // LDS reads spread over the first half of the chunk, DMA issues over the
+    // first three quarters.
+    constexpr int kDma = C::kLoadsPerWave + (kIssueSuper ? C::kSuperLoads : 0);
+    constexpr int kLdsEvery = (C::kMfma / 2) / C::kLdsReads;
+    constexpr int kDmaEvery = (3 * C::kMfma / 4) / kDma;
+#pragma unroll
+    for (int i = 0; i < C::kMfma; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, C::kValuPerMfma, 0);         // VALU
+      if (i % kLdsEvery == kLdsEvery - 1 && i / kLdsEvery < C::kLdsReads)
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                     // LDS read
+      if (i % kDmaEvery == 0 && i / kDmaEvery < kDma)
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                     // VMEM (DMA)
+    }
+  };
+  using Pos0 = std::integral_constant<int, 0>;
+  using Pos1 = std::integral_constant<int, 1>;
+  using Pos2 = std::integral_constant<int, 2>;
+  using Pos3 = std::integral_constant<int, 3>;
+
+  if constexpr (C::kSuper) {
+    issue_super(0);                          // before chunk 0's codes: landed with them
+    __builtin_amdgcn_sched_barrier(0);       // keep that order (the waits count loads in issue order)
+  }
+#pragma unroll
+  for (int s = 0; s < kStages; ++s) issue(s);
+  __builtin_amdgcn_s_waitcnt(C::kWaitFirst);
+  __builtin_amdgcn_s_barrier();
+  Regs cur, nxt;
+  read_stage(cur, 0);
+  scales(cur);
+  decode_step(cur, 0, 0);
+  if constexpr (C::kSuper) {
+    // p.chunks % 4 == 0 (K % 256 == 0).
+    for (uint32_t c = 0; c < p.chunks; c += 4) {
+      step(c, cur, nxt, Pos0{});
+      step(c + 1, nxt, cur, Pos1{});
+      step(c + 2, cur, nxt, Pos2{});
+      step(c + 3, nxt, cur, Pos3{});
+    }
+  } else {
+    for (uint32_t c = 0; c < p.chunks; ++c) {
+      step(c, cur, nxt, Pos0{});
+      cur = nxt;
+    }
+  }
+  // Drain the DMA of the chunks past the end before the workgroup exits.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, tm * BM + wm * FM * 32, p.n_off + tn * BN + wn * FN * 32, r, h);
+}
+
+// Output columns [n_begin, n_end) (n_begin a multiple of 32).
+template <class C, bool kF32Out>
+static hipError_t launch_lds_as(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end,
+                                hipStream_t stream) {
+  p.n_off = n_begin;
+  p.tiles_m = (p.M + C::BM - 1) / C::BM;
+  p.tiles_n = (n_end - n_begin + C::BN - 1) / C::BN;
+  const dim3 grid(p.tiles_m * p.tiles_n), block(C::kThreads);
+  hipLaunchKernelGGL((gemm_lds_kernel<C, kF32Out>), grid, block, C::kLdsBytes, stream, o.a_codes, o.a_scales, o.a_g,
+                     o.w_packed, o.w_g, o.y, p);
+  return hipGetLastError();
+}
+
+template <class C>
+static hipError_t launch_lds(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end, bool out_f32,
+                             hipStream_t stream) {
+  return out_f32 ? launch_lds_as<C, true>(o, p, n_begin, n_end, stream)
+                 : launch_lds_as<C, false>(o, p, n_begin, n_end, stream);
+}
+
+}  // namespace nvfp4

@@ -46,6 +46,10 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
                        const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
                        int64_t ldy, bool out_f32, hipStream_t stream);
 
+// Name of launch `part` (0 or 1) of launch_gemm for this shape on the
+// current device; NULL if that launch does not exist.
+const char* gemm_kernel_for(int64_t M, int64_t N, int64_t K, int part);
+
 hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                                  int64_t M, int64_t K, const void* w_packed, int64_t H, const float* w_g,
                                  const float* a_log, const float* dt_bias, void* y, int64_t ldy,

@@ -1,0 +1,230 @@
+// Activation quantization fused into the narrow NVFP4 GEMM
+// (nvfp4_quantize_gemm).
+#include "gemm_common.h"
+
+namespace nvfp4 {
+
+// ------------------------------------------- fused quantize + tall-skinny GEMM
+//
+// For narrow outputs (N <= 128: the gate projections), the activation is
+// quantized inside the GEMM: each lane loads the 32 bf16 values it supplies
+// to the MFMA (row r, reduction indices [32h, 32h + 32) of the chunk: two
+// whole blocks), quantizes them with the same device code as the stand-alone
+// quantizer (so the codes are identical), optionally stores the codes and
+// scales, and feeds the decoded values to the MFMA; X is read once and the
+// codes never travel through memory.  Tile: 32 rows x FN fragments, the KS
+// waves of a workgroup split the reduction (wave w takes chunks w, w + KS,
+// ...), operands go straight to registers one chunk ahead, and the partial
+// sums meet in LDS (splitk_epilogue).  G_A is read (static) or formed from
+// the amax pass's partial maxima (dynamic; workgroup 0 writes it out), and
+// the epilogue uses the value, not the memory.  K % 64 == 0.
+struct QuantGemmArgs {
+  const uint16_t* x;
+  uint32_t x_bytes, ldx_bytes;
+  float* g_enc;
+  const float* partial;
+  uint32_t n_partial;
+  uint8_t* codes;
+  uint8_t* scales;
+};
+
+template <int KS, int FM, int FN, int kDepth, bool kDynamic, bool kF32Out, bool kCodes>
+__global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q, const uint8_t* __restrict__ w_packed,
+                                                            const float* __restrict__ w_g, void* __restrict__ y,
+                                                            GemmParams p) {
+  __shared__ floatx16 part[KS * 64];
+  __shared__ uint32_t red[KS];
+  const uint32_t lane = threadIdx.x & 63, wave = wave_index();
+  const uint32_t r = lane & 31, h = lane >> 5;
+  float g;
+  if (kDynamic) {
+    uint32_t m = 0;
+    for (uint32_t i = threadIdx.x; i < q.n_partial; i += KS * 64) {
+      const uint32_t v = __float_as_uint(q.partial[i]);
+      m = m > v ? m : v;                       // non-negative floats order as integers
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const uint32_t o = __shfl_xor(m, off, 64);
+      m = m > o ? m : o;
+    }
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    m = red[0];
+#pragma unroll
+    for (int w = 1; w < KS; ++w) m = m > red[w] ? m : red[w];
+    g = global_scale(__uint_as_float(m));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *q.g_enc = g;
+  } else {
+    g = *q.g_enc;
+  }
+  const float gd6 = g * (1.0f / 6.0f);
+  uint32_t tm, tn;
+  tile_of<8>(p, tm, tn);
+  const uint32_t m0 = tm * (FM * 32), n0 = tn * (FN * 32);
+
+  // Per-lane offsets; the chunk goes in the scalar offset.  Rows >= M read
+  // zeros (an all-zero block quantizes to zero codes and is not stored).
+  const __amdgpu_buffer_rsrc_t rx = rsrc(q.x, q.x_bytes);
+  uint32_t x_off[FM];
+#pragma unroll
+  for (int f = 0; f < FM; ++f) {
+    const uint32_t row = m0 + f * 32 + r;
+    x_off[f] = row < p.M ? row * q.ldx_bytes + h * 64u : kOOB;
+  }
+  uint32_t b_off[FN], bs_off[FN];
+#pragma unroll
+  for (int f = 0; f < FN; ++f) {
+    const uint32_t nt = (n0 >> 5) + f;
+    b_off[f] = nt < p.w_tiles ? nt * p.w_kc * 1024u + lane * 16u : kOOB;
+    bs_off[f] = nt < p.w_tiles ? nt * p.w_kc * 128u + r * 4u + h * 2u : kOOB;
+  }
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_packed + p.w_scale_offset, p.w_bytes - p.w_scale_offset);
+  const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
+  float alpha[FN];
+  segment_alpha<FN>(p, g, w_g, n0, r, alpha);
+
+  struct Chunk {
+    int4v x[FM][4];         // per fragment, the lane's 32 bf16 values
+    int4v b[FN];
+    uint32_t sb[FN];        // low 16 bits: the lane's two weight block scales
+  };
+  auto load = [&](Chunk& c, uint32_t i) {
+    const uint32_t kc = wave + KS * i;
+#pragma unroll
+    for (int f = 0; f < FM; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        c.x[f][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, x_off[f] + 16u * j, kc * 128u, 0);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      c.b[f] = __builtin_amdgcn_raw_buffer_load_b128(rb, b_off[f], kc * 1024u, 0);
+      c.sb[f] = __builtin_amdgcn_raw_buffer_load_b16(rbs, bs_off[f], kc * 128u, 0);
+    }
+  };
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int fa = 0; fa < FM; ++fa)
+#pragma unroll
+    for (int fb = 0; fb < FN; ++fb) acc[fa][fb] = floatx16{};
+
+  auto run = [&](auto huge_tag) {
+    constexpr bool kHuge = decltype(huge_tag)::value;
+    auto compute = [&](const Chunk& c, uint32_t i) {
+      const uint32_t kc = wave + KS * i;
+      uint32_t cd[FM][4];
+      half2v sa[FM];
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        const uint32_t v0[8] = {(uint32_t)c.x[f][0][0], (uint32_t)c.x[f][0][1], (uint32_t)c.x[f][0][2],
+                                (uint32_t)c.x[f][0][3], (uint32_t)c.x[f][1][0], (uint32_t)c.x[f][1][1],
+                                (uint32_t)c.x[f][1][2], (uint32_t)c.x[f][1][3]};
+        const uint32_t v1[8] = {(uint32_t)c.x[f][2][0], (uint32_t)c.x[f][2][1], (uint32_t)c.x[f][2][2],
+                                (uint32_t)c.x[f][2][3], (uint32_t)c.x[f][3][0], (uint32_t)c.x[f][3][1],
+                                (uint32_t)c.x[f][3][2], (uint32_t)c.x[f][3][3]};
+        const uint32_t s0 = quantize_block<kHuge>(v0, g, gd6, cd[f][0], cd[f][1]);
+        const uint32_t s1 = quantize_block<kHuge>(v1, g, gd6, cd[f][2], cd[f][3]);
+        const uint32_t row = m0 + f * 32 + r;
+        if (kCodes && row < p.M) {
+          *reinterpret_cast<uint4*>(q.codes + (size_t)row * (p.K >> 1) + kc * 32u + h * 16u) =
+              make_uint4(cd[f][0], cd[f][1], cd[f][2], cd[f][3]);
+          *reinterpret_cast<uint16_t*>(q.scales + (size_t)row * (p.K >> 4) + kc * 4u + h * 2u) =
+              (uint16_t)(s0 | (s1 << 8));
+        }
+        sa[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s0 | (s1 << 8), 1.0f, false);
+      }
+      half2v sb[FN];
+#pragma unroll
+      for (int f = 0; f < FN; ++f) sb[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(c.sb[f], 1.0f, false);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        half8 bv[FN];
+#pragma unroll
+        for (int f = 0; f < FN; ++f)
+          bv[f] = decode8((uint32_t)c.b[f][j], j >> 1 ? __builtin_shufflevector(sb[f], sb[f], 1, 1)
+                                                      : __builtin_shufflevector(sb[f], sb[f], 0, 0));
+#pragma unroll
+        for (int fa = 0; fa < FM; ++fa) {
+          const half8 av = decode8(cd[fa][j], j >> 1 ? __builtin_shufflevector(sa[fa], sa[fa], 1, 1)
+                                                     : __builtin_shufflevector(sa[fa], sa[fa], 0, 0));
+#pragma unroll
+          for (int fb = 0; fb < FN; ++fb)
+            acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv[fb], acc[fa][fb], 0, 0, 0);
+        }
+      }
+    };
+    // Register ring of kDepth + 1 chunks: chunk i + kDepth is loaded while
+    // chunk i is computed (the loop unrolled over the ring's slots).
+    constexpr int kRing = kDepth + 1;
+    Chunk ring[kRing];
+#pragma unroll
+    for (int u = 0; u < kDepth; ++u)
+      if ((uint32_t)u < n_mine) load(ring[u], u);
+    for (uint32_t i = 0; i < n_mine; i += kRing) {
+#pragma unroll
+      for (int u = 0; u < kRing; ++u) {
+        if (i + u < n_mine) {
+          if (i + u + kDepth < n_mine) load(ring[(u + kDepth) % kRing], i + u + kDepth);
+          compute(ring[u], i + u);
+        }
+      }
+    }
+  };
+  if (g > kHugeScale)
+    run(std::integral_constant<bool, true>{});
+  else
+    run(std::integral_constant<bool, false>{});
+  splitk_epilogue<KS, FM, FN, 1, kF32Out, false>(acc, part, p, alpha, y, m0, n0, wave, lane);
+}
+
+template <int KS, int FM, int FN, int kDepth>
+static hipError_t launch_quant_gemm_fn(const QuantGemmArgs& q, bool dynamic, const uint8_t* w_packed,
+                                       const float* w_g, void* y, GemmParams p, bool out_f32,
+                                       hipStream_t stream) {
+  p.tiles_m = (p.M + FM * 32 - 1) / (FM * 32);
+  p.tiles_n = (p.N + FN * 32 - 1) / (FN * 32);
+  const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
+#define NVFP4_QG(D, F32, CODES)                                                                           \
+  hipLaunchKernelGGL((quant_gemm_kernel<KS, FM, FN, kDepth, D, F32, CODES>), grid, block, 0, stream, q, w_packed, w_g, y, p)
+  const bool codes = q.codes != nullptr;
+  if (dynamic) {
+    if (out_f32) { if (codes) NVFP4_QG(true, true, true); else NVFP4_QG(true, true, false); }
+    else { if (codes) NVFP4_QG(true, false, true); else NVFP4_QG(true, false, false); }
+  } else {
+    if (out_f32) { if (codes) NVFP4_QG(false, true, true); else NVFP4_QG(false, true, false); }
+    else { if (codes) NVFP4_QG(false, false, true); else NVFP4_QG(false, false, false); }
+  }
+#undef NVFP4_QG
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* g_enc, bool dynamic,
+                             float* partial, const void* w_packed, int64_t N, const int64_t* seg_offsets,
+                             int n_seg, const float* w_g, uint8_t* codes, uint8_t* scales, void* y, int64_t ldy,
+                             bool out_f32, hipStream_t stream) {
+  if (M == 0) {   // G as the quantizer writes it for an empty tensor
+    if (!dynamic) return hipSuccess;
+    return launch_act_quant(x, 0, K, ldx, codes, scales, g_enc, true, partial, stream);
+  }
+  QuantGemmArgs q{};
+  q.x = static_cast<const uint16_t*>(x);
+  q.x_bytes = (uint32_t)(M * ldx * 2);
+  q.ldx_bytes = (uint32_t)(ldx * 2);
+  q.g_enc = g_enc;
+  q.partial = partial;
+  q.codes = codes;
+  q.scales = scales;
+  if (dynamic) {
+    int n_partial = 0;
+    hipError_t e = launch_act_amax(x, M, K, ldx, partial, &n_partial, stream);
+    if (e != hipSuccess) return e;
+    q.n_partial = (uint32_t)n_partial;
+  }
+  GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
+  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
+  if (N <= 96) return launch_quant_gemm_fn<4, 2, 3, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
+  return launch_quant_gemm_fn<4, 1, 4, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
+}
+
+}  // namespace nvfp4

@@ -79,7 +79,7 @@ def alloc_act(m, k, device) -> QuantizedAct:
 
 
 def act_workspace(m, k, device):
-    return torch.empty(_c.nvfp4_quantize_act_workspace_bytes(m, k), dtype=torch.uint8, device=device)
+    return torch.empty(_c.nvfp4_quantize_act_workspace(m, k), dtype=torch.uint8, device=device)
 
 
 def quantize_act(x, g=None, out: QuantizedAct = None, workspace=None, stream=None) -> QuantizedAct:
@@ -113,10 +113,15 @@ def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None,
     if aq.k != pw.k:
         raise ValueError("K mismatch between activation and weight")
     y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=aq.codes.device)
-    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    kind = _c.NVFP4_F32 if y.dtype == torch.float32 else _c.NVFP4_BF16
     _c.nvfp4_gemm(aq.codes, aq.scales, aq.g, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, kind,
                   stream, M=aq.m, K=aq.k)
     return y
+
+
+def gemm_kernels(m, n, k):
+    """Names of the kernels gemm() launches for an m x n x k call."""
+    return [name for name in (_c.nvfp4_gemm_kernel(m, n, k, part) for part in (0, 1)) if name is not None]
 
 
 def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype=torch.bfloat16, out=None,
@@ -126,7 +131,7 @@ def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype
     if pw.seg_offsets != [0, h, 2 * h]:
         raise ValueError("the gate weight must be packed as two segments [b; a] of equal width")
     y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=aq.codes.device)
-    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    kind = _c.NVFP4_F32 if y.dtype == torch.float32 else _c.NVFP4_BF16
     _c.nvfp4_gemm_gdn_gates(aq.codes, aq.scales, aq.g, pw.packed, h, pw.g_seg, a_log, dt_bias, y, kind, stream,
                             M=aq.m, K=aq.k)
     return y
@@ -143,7 +148,7 @@ def quantize_gemm(x, pw: PackedWeight, g=None, out_dtype=torch.bfloat16, out=Non
         raise ValueError("K mismatch between activation and weight")
     dev = _dev(x)
     y = out if out is not None else torch.empty((m, pw.n), dtype=out_dtype, device=dev)
-    kind = _c.NVFP4_OUT_F32 if y.dtype == torch.float32 else _c.NVFP4_OUT_BF16
+    kind = _c.NVFP4_F32 if y.dtype == torch.float32 else _c.NVFP4_BF16
     gbuf = act_out.g if act_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
     codes = act_out.codes if act_out is not None else None
     scales = act_out.scales if act_out is not None else None

@@ -20,17 +20,17 @@ NVFP4_EHIP = 4
 
 NVFP4_DYNAMIC = 0
 NVFP4_STATIC = 1
-NVFP4_OUT_BF16 = 0
-NVFP4_OUT_F32 = 1
+NVFP4_BF16 = 0
+NVFP4_F32 = 1
 NVFP4_BLOCK = 16
 NVFP4_MAX_SEGMENTS = 8
 
 # name -> (restype, argtypes), in the order of include/nvfp4.h
 _c_int64, _vp, _sz, _int = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
 SIGNATURES = {
-    "nvfp4_status_string": (ctypes.c_char_p, [_int]),
+    "nvfp4_status_str": (ctypes.c_char_p, [_int]),
     "nvfp4_last_hip_error": (_int, []),
-    "nvfp4_quantize_act_workspace_bytes": (_sz, [_c_int64, _c_int64]),
+    "nvfp4_quantize_act_workspace": (_sz, [_c_int64, _c_int64]),
     "nvfp4_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _vp, _vp, _int, _vp, _sz, _vp]),
     "nvfp4_rmsnorm_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, ctypes.c_float, _vp, _vp,
                                            _vp, _vp, _c_int64, _vp]),
@@ -40,6 +40,7 @@ SIGNATURES = {
                                  _vp, _sz, _vp]),
     "nvfp4_unpack_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _vp, _vp]),
     "nvfp4_harmonize_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _int, _vp, _vp, _vp]),
+    "nvfp4_gemm_kernel": (ctypes.c_char_p, [_c_int64, _c_int64, _c_int64, _int]),
     "nvfp4_gemm_gdn_gates": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _vp, _vp, _vp,
                                     _c_int64, _int, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
@@ -53,7 +54,7 @@ _lib = None
 
 class Nvfp4Error(RuntimeError):
     def __init__(self, status, where):
-        msg = lib().nvfp4_status_string(status).decode()
+        msg = lib().nvfp4_status_str(status).decode()
         if status == NVFP4_EHIP:
             msg += " (hipError %d)" % lib().nvfp4_last_hip_error()
         super().__init__("%s: %s" % (where, msg))
@@ -95,8 +96,8 @@ def _offsets(seg_offsets):
     return arr, len(seg_offsets) - 1
 
 
-def nvfp4_quantize_act_workspace_bytes(M, K):
-    return lib().nvfp4_quantize_act_workspace_bytes(int(M), int(K))
+def nvfp4_quantize_act_workspace(M, K):
+    return lib().nvfp4_quantize_act_workspace(int(M), int(K))
 
 
 def nvfp4_packed_weight_bytes(N, K):
@@ -111,7 +112,7 @@ def nvfp4_quantize_act(x, codes, scales, g_enc, mode=NVFP4_DYNAMIC, workspace=No
                        M=None, K=None, ldx=None):
     """x: bf16 [M, K] (row stride ldx); codes uint8 [M, K/2]; scales uint8
     [M, K/16]; g_enc float32 [1]; workspace uint8 of
-    nvfp4_quantize_act_workspace_bytes bytes (dynamic mode)."""
+    nvfp4_quantize_act_workspace bytes (dynamic mode)."""
     M = x.shape[0] if M is None else M
     K = x.shape[1] if K is None else K
     ldx = x.stride(0) if ldx is None else ldx
@@ -159,7 +160,7 @@ def nvfp4_harmonize_weight(packed, N, K, seg_offsets, g_enc_seg, g_shared, strea
 
 
 def nvfp4_gemm(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y,
-               y_dtype=NVFP4_OUT_BF16, stream=None, M=None, K=None):
+               y_dtype=NVFP4_BF16, stream=None, M=None, K=None):
     """Y [M, N] (row stride y.stride(0)) = dq(A) dq(W)^T with per-segment
     global scales."""
     M = a_codes.shape[0] if M is None else M
@@ -171,8 +172,15 @@ def nvfp4_gemm(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg
     _check(st, "nvfp4_gemm")
 
 
+def nvfp4_gemm_kernel(M, N, K, part=0):
+    """Name of launch `part` of nvfp4_gemm for this shape on the current
+    device, or None."""
+    r = lib().nvfp4_gemm_kernel(int(M), int(N), int(K), int(part))
+    return None if r is None else r.decode()
+
+
 def nvfp4_gemm_gdn_gates(a_codes, a_scales, a_g_enc, w_packed, H, w_g_enc_seg, a_log, dt_bias, y,
-                         y_dtype=NVFP4_OUT_BF16, stream=None, M=None, K=None):
+                         y_dtype=NVFP4_BF16, stream=None, M=None, K=None):
     """y [M, 2H] = (beta | alpha) of the fused b|a gate projection."""
     M = a_codes.shape[0] if M is None else M
     K = 2 * a_codes.shape[1] if K is None else K
@@ -183,7 +191,7 @@ def nvfp4_gemm_gdn_gates(a_codes, a_scales, a_g_enc, w_packed, H, w_g_enc_seg, a
 
 
 def nvfp4_quantize_gemm(x, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y, mode=NVFP4_DYNAMIC,
-                        workspace=None, a_codes=None, a_scales=None, y_dtype=NVFP4_OUT_BF16, stream=None):
+                        workspace=None, a_codes=None, a_scales=None, y_dtype=NVFP4_BF16, stream=None):
     """Y [M, N] = quantize(x) then the segment-scaled GEMM, fused (N <= 128);
     x bf16 [M, K] (row stride x.stride(0)); optional a_codes / a_scales
     outputs."""

@@ -36,13 +36,13 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings():
     lib = C.lib()
     for s in range(5):
-        assert lib.nvfp4_status_string(s).decode().startswith("NVFP4")
+        assert lib.nvfp4_status_str(s).decode().startswith("NVFP4")
     assert lib.nvfp4_last_hip_error() == 0
 
 
 def test_sizes():
     lib = C.lib()
-    assert lib.nvfp4_quantize_act_workspace_bytes(8192, 5120) >= 4
+    assert lib.nvfp4_quantize_act_workspace(8192, 5120) >= 4
     # N padded to 32, K to 64: codes Np*Kp/2 + scales Np*Kp/16
     assert lib.nvfp4_packed_weight_bytes(96, 5120) == 96 * 5120 // 2 + 96 * 5120 // 16
     assert lib.nvfp4_packed_weight_bytes(100, 80) == 128 * 128 // 2 + 128 * 128 // 16
@@ -59,7 +59,7 @@ def _offs(lst):
 
 def test_quantize_act_rejects_bad_arguments():
     f = C.lib().nvfp4_quantize_act
-    ws = C.lib().nvfp4_quantize_act_workspace_bytes(4, 32)
+    ws = C.lib().nvfp4_quantize_act_workspace(4, 32)
     ok = dict(x=FAKE, M=4, K=32, ldx=32, codes=FAKE, scales=FAKE, g=FAKE, mode=0, ws=FAKE, wsb=ws)
 
     def call(**kw):
@@ -202,9 +202,41 @@ def test_quantize_gemm_rejects_bad_arguments():
     assert call(codes=FAKE) == C.NVFP4_EINVAL        # codes without scales
     assert call(codes=FAKE + 4, scales=FAKE) == C.NVFP4_EINVAL
     assert call(ldy=95) == C.NVFP4_EINVAL
-    assert call(nseg=3) == C.NVFP4_EINVAL            # table ends past N
+    assert call(segs=_offs([0, 48, 96, 120]), nseg=3) == C.NVFP4_EINVAL   # table ends past N
     assert call(y=FAKE + 1) == C.NVFP4_EINVAL
     assert call(mode=C.NVFP4_DYNAMIC) == C.NVFP4_EINVAL          # no workspace
     assert call(mode=C.NVFP4_DYNAMIC, ws=FAKE, wsb=4) == C.NVFP4_EWORKSPACE
     assert call(N=160, segs=_offs([0, 160]), nseg=1, ldy=160) == C.NVFP4_EUNSUPPORTED   # N > 128
     assert call(K=80, ldx=80) == C.NVFP4_EUNSUPPORTED             # K % 64 != 0
+
+
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:
+        return True
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="runs where there is no GPU: valid arguments stop at the device check")
+def test_valid_arguments_stop_at_the_device_check():
+    lib = C.lib()
+    ws = lib.nvfp4_quantize_act_workspace(64, 256)
+    offs = _offs([0, 48, 96])
+    calls = [
+        lambda: lib.nvfp4_quantize_act(FAKE, 64, 256, 256, FAKE, FAKE, FAKE, C.NVFP4_DYNAMIC, FAKE, ws, None),
+        lambda: lib.nvfp4_rmsnorm_quantize_act(FAKE, 64, 256, 256, FAKE, 1e-6, FAKE, FAKE, FAKE, None, 0, None),
+        lambda: lib.nvfp4_pack_weight(FAKE, 96, 256, 256, offs, 2, FAKE, C.NVFP4_STATIC,
+                                      FAKE, lib.nvfp4_packed_weight_bytes(96, 256), None, 0, None),
+        lambda: lib.nvfp4_unpack_weight(FAKE, 96, 256, FAKE, FAKE, None),
+        lambda: lib.nvfp4_harmonize_weight(FAKE, 96, 256, offs, 2, FAKE, FAKE + 64, None),
+        lambda: lib.nvfp4_gemm(FAKE, FAKE, FAKE, 64, 256, FAKE, 96, offs, 2, FAKE, FAKE, 96, C.NVFP4_BF16, None),
+        lambda: lib.nvfp4_gemm_gdn_gates(FAKE, FAKE, FAKE, 64, 256, FAKE, 48, FAKE, FAKE, FAKE, FAKE, 96,
+                                         C.NVFP4_F32, None),
+        lambda: lib.nvfp4_quantize_gemm(FAKE, 64, 256, 256, FAKE, C.NVFP4_STATIC, None, 0, FAKE, 96, offs, 2, FAKE,
+                                        None, None, FAKE, 96, C.NVFP4_BF16, None),
+    ]
+    for call in calls:
+        assert call() in (C.NVFP4_EHIP, C.NVFP4_EUNSUPPORTED)
+    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 0) is None
+    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 2) is None

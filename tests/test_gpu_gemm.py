@@ -90,12 +90,14 @@ def test_gemm_ragged_shapes(m, n, k, offs):
     check_small(x, w, offs, what="%dx%dx%d" % (m, n, k))
 
 
-def test_gemm_tail_columns_as_narrow_tiles():
+@pytest.mark.parametrize("k", [128, 512])
+def test_gemm_tail_columns_as_narrow_tiles(k):
     # 2 x 130 tiles of 256 x 256: on a 256-CU device the 4 tiles past two
     # full rounds (two tile columns) run as 256 x 128 tiles in a second
-    # launch; ragged M and N inside that tail.  Every element is checked.
-    rng = np.random.default_rng(304)
-    m, n, k = 300, 129 * 256 + 100, 128
+    # launch; ragged M and N inside that tail.  K = 512 runs the scale
+    # super-stage kernel for the first launch.  Every element is checked.
+    rng = np.random.default_rng(304 + k)
+    m, n = 300, 129 * 256 + 100
     x, w = _xw(rng, m, n, k)
     offs = [0, 20000, 33000, n]
     y32, y16, _, _ = run_gpu(x, w, offs)
@@ -103,9 +105,28 @@ def test_gemm_tail_columns_as_narrow_tiles():
     wp, ws, gw = OQ.quantize_segments(w, offs)
     y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs)
     r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
-    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "tail split")
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "tail split K=%d" % k)
     np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
                                   bf16_rne_of(y32.contiguous()))
+    log("tail split K=%d: launches %s" % (k, L.gemm_kernels(m, n, k)))
+
+
+def test_gemm_super_stage_every_element():
+    # The scale super-stage kernel (K % 256 == 0) over 5 x 6 tiles with
+    # ragged M and N, 32 chunks (8 super-stages), every element checked.
+    rng = np.random.default_rng(305)
+    m, n, k = 1100, 1500, 2048
+    x, w = _xw(rng, m, n, k)
+    offs = [0, 700, 1500]
+    y32, y16, _, _ = run_gpu(x, w, offs)
+    xp, xs, gx = OQ.quantize_tensor(x)
+    wp, ws, gw = OQ.quantize_segments(w, offs)
+    y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs)
+    r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "super-stage")
+    np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_of(y32.contiguous()))
+    assert "Super" in L.gemm_kernels(m, n, k)[0]
 
 
 def test_gemm_strided_output():
@@ -149,11 +170,19 @@ def test_gemm_is_deterministic_and_stays_in_bounds():
     assert torch.all(pad == 12345.0) and torch.all(buf[200 * 168:] == 12345.0)
 
 
-def _sample_rows(m, rng):
+def _sample_rows(m, tile):
+    """Rows checked on a full workload: every row if m <= 32; else one row
+    in every `tile`-row M-tile of the kernel (its position within the tile
+    rotating with the tile index), all rows of the middle tile band, and the
+    first and last 8 rows."""
     if m <= 32:
         return np.arange(m)
-    rows = list(range(8)) + list(range(m - 8, m)) + list(rng.choice(np.arange(8, m - 8), 16, replace=False))
-    return np.array(sorted(set(rows)))
+    tiles = (m + tile - 1) // tile
+    rows = [t * tile + (t * 37 + 5) % tile for t in range(tiles)]
+    mid = tiles // 2
+    rows += list(range(mid * tile, min(m, (mid + 1) * tile)))
+    rows += list(range(8)) + list(range(m - 8, m))
+    return np.array(sorted(set(r for r in rows if r < m)))
 
 
 @pytest.mark.parametrize("name", synth.CONFIG_ORDER + synth.DECODE_ORDER)
@@ -165,8 +194,11 @@ def test_gemm_full_workloads(name):
     assert np.float32(aq.g.item()) == wl["gx"]
     # BF16 output is the RNE of the FP32 output, everywhere.
     assert torch.equal(y16.contiguous().view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
-    rows = _sample_rows(cfg.m, np.random.default_rng(cfg.index))
-    log("%s: oracle on %d sampled rows" % (name, len(rows)))
+    kernels = L.gemm_kernels(cfg.m, cfg.n, cfg.k)
+    tile = 64 if "64x96" in kernels[0] else (32 if "32x64" in kernels[0] else 256)
+    rows = _sample_rows(cfg.m, tile)
+    log("%s: oracle on %d rows (%d-row tiles: one per tile + a full band), kernels %s" % (
+        name, len(rows), tile, kernels))
     args = (wl["xp"], wl["xs"], wl["gx"], wl["wp"], wl["ws"], wl["gw"], cfg.seg_offsets)
     y_ref = OG.gemm_f64(*args, rows=rows)
     r_ref = OG.abs_bound(*args, rows=rows)

@@ -106,3 +106,68 @@ def test_abs_bound_dominates():
     y = G.gemm_f64(ap, as_, ga, wp, ws, gw, offs)
     r = G.abs_bound(ap, as_, ga, wp, ws, gw, offs)
     assert np.all(np.abs(y) <= r * (1 + 1e-12))
+
+
+def test_abs_bound_equals_y_for_nonnegative_operands():
+    # With every dequantized product >= 0 the sum of |a_k w_k| is the sum
+    # itself, so R must equal Y (segment scales included) on every element.
+    rng = np.random.default_rng(26)
+    m, k, segs = 20, 128, (8, 24, 16)
+    offs = [0] + list(np.cumsum(segs))
+    x = np.abs(rng.standard_normal((m, k)))
+    x[:, 9] *= 150.0
+    w = np.concatenate([np.abs(rng.standard_normal((s, k))) * sd for s, sd in zip(segs, (0.02, 0.5, 3e-3))])
+    ap, as_, ga = Q.quantize_tensor(bits_of(x))
+    wp, ws, gw = Q.quantize_segments(bits_of(w), offs)
+    y = G.gemm_exact(ap, as_, ga, wp, ws, gw, offs)
+    r = G.abs_bound(ap, as_, ga, wp, ws, gw, offs)
+    assert np.all(y > 0)
+    np.testing.assert_allclose(r, y, rtol=1e-14, atol=0)
+
+
+def test_abs_bound_of_one_hot_rows():
+    # Row m of X holds one non-zero value, at position k_m; then
+    # R[m, n] = |x_hat[m, k_m]| * |w_hat[n, k_m]|, with x_hat and w_hat the
+    # dequantized tensors (each divided by its own global scale).
+    rng = np.random.default_rng(27)
+    k, segs = 96, (16, 8, 40)
+    offs = [0] + list(np.cumsum(segs))
+    pos = rng.integers(0, k, 48)
+    x = np.zeros((48, k))
+    x[np.arange(48), pos] = rng.choice([-3.0, -0.5, 1.0, 6.0, 2.0], 48)
+    w = np.concatenate([rng.standard_normal((s, k)) * sd for s, sd in zip(segs, (0.02, 7.0, 1e-3))])
+    ap, as_, ga = Q.quantize_tensor(bits_of(x))
+    wp, ws, gw = Q.quantize_segments(bits_of(w), offs)
+    xh = Q.dequantize(ap, as_, ga)
+    wh = np.concatenate([Q.dequantize(wp[a:b], ws[a:b], gw[s]) for s, (a, b) in enumerate(zip(offs, offs[1:]))])
+    expect = np.abs(xh[np.arange(48), pos])[:, None] * np.abs(wh[:, pos]).T
+    r = G.abs_bound(ap, as_, ga, wp, ws, gw, offs)
+    np.testing.assert_allclose(r, expect, rtol=1e-14, atol=0)
+    assert np.mean(r[:, offs[1]:offs[2]] > 0) > 0.8
+
+
+def test_abs_bound_ignores_signs_and_scales_with_its_segment():
+    # Flipping the sign bit of whole rows of X or W leaves R unchanged (Y
+    # changes sign there); scaling segment s of W by 2^j scales only that
+    # segment's columns of R by 2^j.
+    rng = np.random.default_rng(28)
+    ap, as_, ga, wp, ws, gw, offs, n = _problem(rng)
+    r = G.abs_bound(ap, as_, ga, wp, ws, gw, offs)
+    y = G.gemm_exact(ap, as_, ga, wp, ws, gw, offs)
+    flip_a = np.zeros(ap.shape[0], dtype=bool)
+    flip_a[::3] = True
+    flip_w = np.zeros(n, dtype=bool)
+    flip_w[1::2] = True
+    ap2, wp2 = ap.copy(), wp.copy()
+    ap2[flip_a] ^= 0x88
+    wp2[flip_w] ^= 0x88
+    np.testing.assert_array_equal(G.abs_bound(ap2, as_, ga, wp2, ws, gw, offs), r)
+    sgn = np.where(flip_a, -1.0, 1.0)[:, None] * np.where(flip_w, -1.0, 1.0)[None, :]
+    np.testing.assert_array_equal(G.gemm_exact(ap2, as_, ga, wp2, ws, gw, offs), sgn * y)
+    for s, j in [(0, 4), (2, -6)]:
+        gw2 = list(gw)
+        gw2[s] = np.float32(gw[s] * 2.0 ** -j)
+        r2 = G.abs_bound(ap, as_, ga, wp, ws, gw2, offs)
+        expect = r.copy()
+        expect[:, offs[s]:offs[s + 1]] *= 2.0 ** j
+        np.testing.assert_allclose(r2, expect, rtol=1e-15, atol=0)

@@ -4,7 +4,10 @@
   (random values over the whole bf16 range, subnormals, exact midpoints);
 * closed forms of the norm: a constant row maps to +-gamma, a one-hot row of
   length K to sqrt(K) at the hot position, scaling a row by 2^j changes
-  nothing (eps = 0), and mean(y^2) = 1 for gamma = 1, eps = 0.
+  nothing (eps = 0), and mean(y^2) = 1 for gamma = 1, eps = 0;
+* where eps enters: a constant row c with eps = c^2 maps to gamma / sqrt(2),
+  a one-hot row 8 e_k of length 64 with eps = 3 to 4 gamma_k, and a zero row
+  with eps > 0 to zeros.
 """
 
 from fractions import Fraction
@@ -80,3 +83,30 @@ def test_power_of_two_scaling_and_unit_rms():
         np.testing.assert_array_equal(ON.rmsnorm_bf16(_bits(x * 2.0 ** j), gamma, 0.0), y0)
     yf = ON.rmsnorm_f64(_bits(x), gamma, 0.0)
     np.testing.assert_allclose(np.mean(yf * yf, axis=1), 1.0, rtol=1e-12)
+
+
+def test_eps_inside_the_square_root():
+    # y = x / sqrt(mean x^2 + eps) * gamma: a constant row c with eps = c^2
+    # gives c / sqrt(2 c^2) = 1 / sqrt(2) times gamma.
+    rng = np.random.default_rng(6)
+    gamma = _bits(rng.uniform(0.5, 2.0, 128))
+    g = OF.bf16_bits_to_f64(gamma)
+    for c in (0.5, 3.0, 0.0625):
+        y = ON.rmsnorm_f64(_bits(np.full((2, 128), c) * np.array([[1.0], [-1.0]])), gamma, c * c)
+        np.testing.assert_allclose(y[0] * np.sqrt(2.0), g, rtol=1e-15)
+        np.testing.assert_allclose(y[1] * np.sqrt(2.0), -g, rtol=1e-15)
+
+
+def test_eps_with_one_hot_and_zero_rows():
+    # 8 e_k in a row of 64: mean x^2 = 1, so with eps = 3 the hot value maps
+    # to 8 / sqrt(4) = 4 times gamma_k.  A zero row with eps > 0 maps to 0.
+    rng = np.random.default_rng(7)
+    gamma = _bits(rng.uniform(0.5, 2.0, 64))
+    g = OF.bf16_bits_to_f64(gamma)
+    x = np.zeros((3, 64), dtype=np.uint16)
+    x[0, 11] = _bits(8.0)
+    x[1, 0] = _bits(-8.0)
+    y = ON.rmsnorm_f64(x, gamma, 3.0)
+    assert y[0, 11] == 4.0 * g[11] and y[1, 0] == -4.0 * g[0]
+    assert np.count_nonzero(y[:2]) == 2
+    assert np.all(y[2] == 0.0) and np.all(np.isfinite(y))

@@ -169,8 +169,9 @@ def test_scale_is_monotone_in_block_max():
 
 
 def test_outlier_degrades_only_its_own_block():
-    # Section 2: a block's largest value fixes its scale, so an outlier changes
-    # only its own block (with the global scale held fixed).
+    # Section 2 (NVFP4): with G held fixed, each block's scale and codes depend
+    # on that block's 16 values alone; planting a large value in one block
+    # must leave every other block's bytes as they were.
     rng = np.random.default_rng(15)
     x = rng.standard_normal((6, 128))
     g = np.float32(5.0)
