@@ -105,6 +105,26 @@ int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nvfp4_quantize_act without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments (minus the workspace),
+ * same kernels, same results as nvfp4_quantize_act.
+ *
+ * The dynamic global scale's partial maxima go to a scratch array of
+ * 4096 bytes per device, which the library holds from its first call on that
+ * device until the process ends.  The call allocates nothing and calls no
+ * allocating routine.  Every call on a device shares that device's scratch:
+ * calls that overlap on one GPU race (order them, e.g. on one stream); calls
+ * on different GPUs do not interact.  Its contents between calls do not
+ * matter (nothing in it needs to start at zero).
+ * Errors: as nvfp4_quantize_act; NVFP4_EWORKSPACE if the call would need more
+ * scratch than 4096 bytes (no current shape does).
+ */
+int nvfp4_quantize_act_noalloc(const void* x, int64_t M, int64_t K, int64_t ldx,
+                               uint8_t* codes, uint8_t* scales, float* g_enc,
+                               int mode, void* stream);
+
+/*
  * RMSNorm fused with activation quantization under a calibrated (static)
  * global scale: one pass over the activations (the paper serves its W4A4
  * model with activation scales calibrated offline, section 3 "Checkpoints";

@@ -14,8 +14,18 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "launch.h"
 #include "quant_device.h"
+
+// Scratch memory of the allocation-free entry point
+// (nvfp4_quantize_act_noalloc): the dynamic global scale's partial maxima,
+// kActScratchBytes per device, held until the process ends.  Host code never
+// uses this name as an address (it names a host-side stand-in); it takes the
+// device address from hipGetSymbolAddress, once per device (act_scratch).
+static __device__ __align__(256) float scratch[nvfp4::kActPartials];
+static_assert(sizeof(scratch) == nvfp4::kActScratchBytes, "scratch size");
 
 namespace nvfp4 {
 
@@ -219,6 +229,29 @@ hipError_t launch_act_amax(const void* x, int64_t M, int64_t K, int64_t ldx, flo
     hipLaunchKernelGGL(amax_partial_kernel<false>, dim3(*n_partial), dim3(kThreads), 0, stream, xp, n_vec,
                        vec_per_row, (uint32_t)ldx, partial);
   return hipGetLastError();
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+float* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+}  // namespace
+
+hipError_t act_scratch(float** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  // Once per device, with that device current (the calling thread's).
+  std::call_once(g_scratch_once[dev], [dev]() {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,

@@ -81,29 +81,57 @@ size_t nvfp4_quantize_act_workspace(int64_t M, int64_t K) {
   return (size_t)nvfp4::kActPartials * sizeof(float);
 }
 
-int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
-                       uint8_t* scales, float* g_enc, int mode, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+// Arguments of nvfp4_quantize_act other than the workspace.
+static int check_act_args(const void* x, int64_t M, int64_t K, int64_t ldx, const uint8_t* codes,
+                          const uint8_t* scales, const float* g_enc, int mode) {
   if (mode != NVFP4_DYNAMIC && mode != NVFP4_STATIC) return NVFP4_EINVAL;
   if (M < 0 || K < 0 || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
   if (g_enc == nullptr || (reinterpret_cast<uintptr_t>(g_enc) & 3u)) return NVFP4_EINVAL;
-  const bool empty = (M == 0 || K == 0);
-  if (!empty) {
+  if (M != 0 && K != 0) {
     if (ldx < K || ldx % 8 != 0) return NVFP4_EINVAL;
     if (M * ldx >= kI32Lim || M * K >= kI32Lim) return NVFP4_EINVAL;
     if (x == nullptr || codes == nullptr || scales == nullptr) return NVFP4_EINVAL;
     if (!aligned16(x) || !aligned16(codes) || !aligned16(scales)) return NVFP4_EINVAL;
   }
+  return NVFP4_OK;
+}
+
+int nvfp4_quantize_act(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
+                       uint8_t* scales, float* g_enc, int mode, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = check_act_args(x, M, K, ldx, codes, scales, g_enc, mode);
+  if (st != NVFP4_OK) return st;
+  const bool empty = (M == 0 || K == 0);
   const bool dynamic = mode == NVFP4_DYNAMIC;
   if (dynamic && !empty) {
     if (workspace == nullptr || !aligned16(workspace)) return NVFP4_EINVAL;
     if (workspace_bytes < nvfp4_quantize_act_workspace(M, K)) return NVFP4_EWORKSPACE;
   }
-  int st = check_device();
+  st = check_device();
   if (st != NVFP4_OK) return st;
   if (empty && !dynamic) return NVFP4_OK;
   hipError_t e = nvfp4::launch_act_quant(x, M, K, ldx, codes, scales, g_enc, dynamic,
                                          static_cast<float*>(workspace),
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
+int nvfp4_quantize_act_noalloc(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
+                               uint8_t* scales, float* g_enc, int mode, void* stream) {
+  int st = check_act_args(x, M, K, ldx, codes, scales, g_enc, mode);
+  if (st != NVFP4_OK) return st;
+  const bool empty = (M == 0 || K == 0);
+  const bool dynamic = mode == NVFP4_DYNAMIC;
+  if (dynamic && nvfp4_quantize_act_workspace(M, K) > nvfp4::kActScratchBytes) return NVFP4_EWORKSPACE;
+  st = check_device();
+  if (st != NVFP4_OK) return st;
+  if (empty && !dynamic) return NVFP4_OK;
+  float* ws = nullptr;
+  if (dynamic && !empty) {
+    hipError_t e = nvfp4::act_scratch(&ws);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  hipError_t e = nvfp4::launch_act_quant(x, M, K, ldx, codes, scales, g_enc, dynamic, ws,
                                          static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }

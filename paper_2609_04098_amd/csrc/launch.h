@@ -12,6 +12,9 @@ namespace nvfp4 {
 
 // Partial maxima written by the activation amax pass (one per workgroup).
 constexpr int kActPartials = 1024;
+// Bytes of the per-device scratch array of the allocation-free quantizer
+// (the partial maxima).
+constexpr size_t kActScratchBytes = kActPartials * sizeof(float);
 // Upper bound on quantize workgroups (grid-strided beyond that).
 constexpr int kActQuantGridCap = 4096;
 // Partial maxima per weight segment.
@@ -20,6 +23,10 @@ constexpr int kWeightPartials = 256;
 hipError_t launch_act_quant(const void* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
                             uint8_t* scales, float* g_enc, bool dynamic, float* partial,
                             hipStream_t stream);
+
+// Device address of the current device's scratch array (kActScratchBytes),
+// taken once per device with hipGetSymbolAddress.
+hipError_t act_scratch(float** ptr);
 
 // Pass 1 of the dynamic quantizer: partial maxima of |x| into `partial`
 // (n_partial <= kActPartials values).

@@ -32,6 +32,7 @@ SIGNATURES = {
     "nvfp4_last_hip_error": (_int, []),
     "nvfp4_quantize_act_workspace": (_sz, [_c_int64, _c_int64]),
     "nvfp4_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _vp, _vp, _int, _vp, _sz, _vp]),
+    "nvfp4_quantize_act_noalloc": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _vp, _vp, _int, _vp]),
     "nvfp4_rmsnorm_quantize_act": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, ctypes.c_float, _vp, _vp,
                                            _vp, _vp, _c_int64, _vp]),
     "nvfp4_packed_weight_bytes": (_sz, [_c_int64, _c_int64]),
@@ -120,6 +121,17 @@ def nvfp4_quantize_act(x, codes, scales, g_enc, mode=NVFP4_DYNAMIC, workspace=No
     st = lib().nvfp4_quantize_act(_ptr(x), M, K, ldx, _ptr(codes), _ptr(scales), _ptr(g_enc), mode,
                                   _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "nvfp4_quantize_act")
+
+
+def nvfp4_quantize_act_noalloc(x, codes, scales, g_enc, mode=NVFP4_DYNAMIC, stream=None, M=None, K=None, ldx=None):
+    """nvfp4_quantize_act without a workspace (the library's per-device
+    scratch holds the partial maxima); same layouts."""
+    M = x.shape[0] if M is None else M
+    K = x.shape[1] if K is None else K
+    ldx = x.stride(0) if ldx is None else ldx
+    st = lib().nvfp4_quantize_act_noalloc(_ptr(x), M, K, ldx, _ptr(codes), _ptr(scales), _ptr(g_enc), mode,
+                                          _stream(stream))
+    _check(st, "nvfp4_quantize_act_noalloc")
 
 
 def nvfp4_rmsnorm_quantize_act(x, gamma, eps, codes, scales, g_enc, y=None, stream=None):

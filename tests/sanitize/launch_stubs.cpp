@@ -12,6 +12,7 @@ hipError_t launch_act_quant(const void*, int64_t, int64_t, int64_t, uint8_t*, ui
                             hipStream_t) {
   return hipErrorNoDevice;
 }
+hipError_t act_scratch(float**) { return hipErrorNoDevice; }
 hipError_t launch_act_amax(const void*, int64_t, int64_t, int64_t, float*, int*, hipStream_t) {
   return hipErrorNoDevice;
 }

@@ -225,6 +225,7 @@ def test_valid_arguments_stop_at_the_device_check():
     offs = _offs([0, 48, 96])
     calls = [
         lambda: lib.nvfp4_quantize_act(FAKE, 64, 256, 256, FAKE, FAKE, FAKE, C.NVFP4_DYNAMIC, FAKE, ws, None),
+        lambda: lib.nvfp4_quantize_act_noalloc(FAKE, 64, 256, 256, FAKE, FAKE, FAKE, C.NVFP4_DYNAMIC, None),
         lambda: lib.nvfp4_rmsnorm_quantize_act(FAKE, 64, 256, 256, FAKE, 1e-6, FAKE, FAKE, FAKE, None, 0, None),
         lambda: lib.nvfp4_pack_weight(FAKE, 96, 256, 256, offs, 2, FAKE, C.NVFP4_STATIC,
                                       FAKE, lib.nvfp4_packed_weight_bytes(96, 256), None, 0, None),
@@ -240,3 +241,21 @@ def test_valid_arguments_stop_at_the_device_check():
         assert call() in (C.NVFP4_EHIP, C.NVFP4_EUNSUPPORTED)
     assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 0) is None
     assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 2) is None
+
+
+def test_quantize_act_noalloc_rejects_bad_arguments():
+    f = C.lib().nvfp4_quantize_act_noalloc
+
+    def call(x=FAKE, M=4, K=32, ldx=32, codes=FAKE, scales=FAKE, g=FAKE, mode=0):
+        return f(x, M, K, ldx, codes, scales, g, mode, None)
+    assert call(K=24) == C.NVFP4_EINVAL
+    assert call(M=-1) == C.NVFP4_EINVAL
+    assert call(ldx=16) == C.NVFP4_EINVAL
+    assert call(x=None) == C.NVFP4_EINVAL
+    assert call(scales=FAKE + 4) == C.NVFP4_EINVAL
+    assert call(g=None) == C.NVFP4_EINVAL
+    assert call(mode=2) == C.NVFP4_EINVAL
+    assert call(M=1 << 20, K=1 << 12, ldx=1 << 12) == C.NVFP4_EINVAL
+    # The scratch (4096 bytes per device) covers every shape's workspace.
+    for m, k in [(1, 16), (8192, 5120), (32768, 5120), (131071, 16384)]:
+        assert C.lib().nvfp4_quantize_act_workspace(m, k) <= 4096
