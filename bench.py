@@ -176,6 +176,54 @@ def measure_workload(name, steps, warmup, dev, log_fn):
     return out
 
 
+def measure_decode(pw, m, steps, warmup, dev):
+    """Decode-shaped calls against the headline's gate/up weight (34816 x
+    5120, two segments): m rows of residual-stream X (the 32-token decode
+    workload's first rows), dynamic G.  Unfused (quantizer + GEMM, two or
+    three launches) and fused (nvfp4_quantize_gemm, one launch).  Before
+    every timed call a 640 MB read evicts the weight from the 256 MB MALL,
+    as successive layers of a model would; HIP events, median."""
+    import numpy as np
+    import torch
+    from paper_2609_04098_amd import linear as L
+    from paper_2609_04098_amd import synth
+
+    cfg = synth.CONFIGS["decode_m32"]
+    xb = synth.make_x(cfg)[:m]
+    x = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).to(dev)
+    stream = torch.cuda.current_stream()
+    aq = L.alloc_act(m, cfg.k, dev)
+    ws = L.act_workspace(m, cfg.k, dev)
+    wsq = L.quantize_gemm_workspace(m, pw.n, cfg.k, dev)
+    y = torch.empty((m, pw.n), dtype=torch.bfloat16, device=dev)
+    flush = torch.ones(160 << 20, dtype=torch.float32, device=dev)
+
+    def unfused():
+        L.quantize_act(x, out=aq, workspace=ws)
+        L.gemm(aq, pw, out=y)
+
+    def fused():
+        L.quantize_gemm(x, pw, out=y, workspace=wsq)
+
+    res = {"M": m, "N": pw.n, "K": cfg.k, "w_bytes": int(pw.packed.numel())}
+    for name, fn in (("unfused", unfused), ("fused", fused)):
+        for _ in range(warmup):
+            fn()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for i in range(steps):
+            flush.sum()
+            evs[i][0].record(stream)
+            fn()
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.median([a.elapsed_time(b) for a, b in evs]))
+        res[name + "_median_ms"] = round(ms, 4)
+        res[name + "_w_gbs"] = round(pw.packed.numel() / (ms * 1e-3) / 1e9, 1)
+        res[name + "_frac_hbm"] = round(pw.packed.numel() / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    del flush
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -396,6 +444,8 @@ def main():
         "gemm_source_sha256_16": gemm_source_hash(),
     }
     if not args.no_other_workloads and args.workload == WORKLOAD:
+        log("decode shapes against the gate/up weight")
+        result["decode"] = {"m%d" % m: measure_decode(pw, m, args.steps, args.warmup, dev) for m in (1, 7, 32)}
         result["other_workloads"] = {}
         for name in ("gdn_qkv", "mlp_down", "ab_gates"):
             result["other_workloads"][name] = measure_workload(name, max(5, args.steps // 2), max(2, args.warmup), dev,

@@ -275,26 +275,42 @@ int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales,
                          const float* a_log, const float* dt_bias,
                          void* y, int64_t ldy, int y_dtype, void* stream);
 
+/* Workspace bytes nvfp4_quantize_gemm needs for an M x N x K call. */
+size_t nvfp4_quantize_gemm_workspace(int64_t M, int64_t N, int64_t K);
+
 /*
- * Activation quantization fused into a narrow GEMM (N <= 128: the
- * tall-skinny gate projections; paper, section 2 for the format, section 6
- * for the fused segments).  The result equals nvfp4_quantize_act followed
- * by nvfp4_gemm: the activation is quantized by the same device code (the
- * same codes, scales and G_A), and the GEMM sums in the same order as
- * nvfp4_gemm at these shapes.  X is read once in static mode (twice in
- * dynamic mode, whose global scale needs all of X first); the codes go to
- * memory only if asked for.
+ * Activation quantization fused into the GEMM, in one call, for the shapes
+ * where a separate quantizer launch costs most (paper, section 2 for the
+ * format, section 6 for the fused segments; section 4 and section 9
+ * "Decode overhead": small-batch activation quantization):
+ *   - narrow outputs, N <= 128 (the tall-skinny gate projections), any M:
+ *     X is quantized in registers inside the GEMM (read once with a given
+ *     G; dynamic mode adds the amax pass in front);
+ *   - decode shapes, M <= 32 (any N): for M * K <= 16384 (up to 3 tokens
+ *     of width 5120) one launch in which every workgroup quantizes all of
+ *     X into its LDS (and takes the dynamic G itself) and the GEMM reads
+ *     the activation from there; larger activations take two launches (the
+ *     quantizer, then the GEMM), with the codes in a_codes or in the
+ *     workspace.
+ * The result equals nvfp4_quantize_act followed by nvfp4_gemm: the same
+ * codes, scales and G_A, and the GEMM sums in the same order as nvfp4_gemm
+ * at these shapes.
  *
  *   x, M, K, ldx   bf16 activation, as for nvfp4_quantize_act.
  *   a_g_enc        one device float: G_A, written (NVFP4_DYNAMIC) or read
  *                  (NVFP4_STATIC), as for nvfp4_quantize_act.
- *   workspace, workspace_bytes   as for nvfp4_quantize_act (dynamic mode).
+ *   workspace, workspace_bytes   device scratch of at least
+ *                  nvfp4_quantize_gemm_workspace(M, N, K) bytes, 16-byte
+ *                  aligned; required in dynamic mode and on the decode path
+ *                  (M <= 32 and N > 128), else unused (may be NULL).  Its
+ *                  contents on entry do not matter; calls sharing one
+ *                  workspace must be ordered.
  *   w_packed, N, seg_offsets, n_seg, w_g_enc_seg, y, ldy, y_dtype
  *                  as for nvfp4_gemm.
  *   a_codes, a_scales   optional outputs ([M x K/2], [M x K/16] as written
  *                  by nvfp4_quantize_act); both NULL or both set.
- * Requirements: those of nvfp4_quantize_act and nvfp4_gemm; N > 128 or
- * K % 64 != 0 gives NVFP4_EUNSUPPORTED.
+ * Requirements: those of nvfp4_quantize_act and nvfp4_gemm; N > 128 with
+ * M > 32, or K % 64 != 0, gives NVFP4_EUNSUPPORTED.
  */
 int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx,
                         float* a_g_enc, int mode, void* workspace, size_t workspace_bytes,

@@ -290,6 +290,11 @@ int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const 
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 
+size_t nvfp4_quantize_gemm_workspace(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 1 || K < 0) return 0;
+  return nvfp4::quant_gemm_workspace_bytes(M, N, K);
+}
+
 int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* a_g_enc, int mode,
                         void* workspace, size_t workspace_bytes, const void* w_packed, int64_t N,
                         const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg, uint8_t* a_codes,
@@ -314,16 +319,16 @@ int nvfp4_quantize_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float*
     const uintptr_t elem = y_dtype == NVFP4_F32 ? 4u : 2u;
     if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
   }
-  if (dynamic) {
+  if (dynamic || nvfp4::quant_gemm_uses_decode_path(M, N)) {
     if (workspace == nullptr || !aligned16(workspace)) return NVFP4_EINVAL;
-    if (workspace_bytes < nvfp4_quantize_act_workspace(M, K)) return NVFP4_EWORKSPACE;
+    if (workspace_bytes < nvfp4_quantize_gemm_workspace(M, N, K)) return NVFP4_EWORKSPACE;
   }
-  if (N > 128 || K % 64 != 0) return NVFP4_EUNSUPPORTED;
+  if ((N > 128 && M > 32) || K % 64 != 0) return NVFP4_EUNSUPPORTED;
   int st = check_device();
   if (st != NVFP4_OK) return st;
-  hipError_t e = nvfp4::launch_quant_gemm(x, M, K, ldx, a_g_enc, dynamic, static_cast<float*>(workspace), w_packed,
-                                          N, seg_offsets, n_seg, w_g_enc_seg, a_codes, a_scales, y, ldy,
-                                          y_dtype == NVFP4_F32, static_cast<hipStream_t>(stream));
+  hipError_t e = nvfp4::launch_quant_gemm(x, M, K, ldx, a_g_enc, dynamic, workspace, w_packed, N, seg_offsets,
+                                          n_seg, w_g_enc_seg, a_codes, a_scales, y, ldy, y_dtype == NVFP4_F32,
+                                          static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 

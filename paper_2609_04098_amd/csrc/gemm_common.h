@@ -128,11 +128,16 @@ __device__ __forceinline__ half8 decode8(uint32_t c, half2v s) {
 // dst + 16 * lane (4 * lane); dst must be the same for the whole wave.
 // The chunk advance goes in the scalar offset soffset; out-of-range per-lane
 // offsets (kOOB) read zeros.
+// Cache-policy operand of a buffer load: device scope (coherent across the
+// XCDs' L2 caches).
+constexpr int kDeviceScope = 16;
+template <int kAux = 0>
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset, uint32_t soffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 16, voffset, soffset, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 16, voffset, soffset, 0, kAux);
 }
+template <int kAux = 0>
 __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint8_t* dst, uint32_t voffset, uint32_t soffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 4, voffset, soffset, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (NVFP4_LDS void*)dst, 4, voffset, soffset, 0, kAux);
 }
 
 // Index of the calling wave in its workgroup, in a scalar register.
@@ -388,6 +393,19 @@ hipError_t launch_lds_tall(const GemmOperands& o, GemmParams p, uint32_t n_begin
 // Split-K: 64 x 96 tiles (N <= 96, optional GDN gate epilogue), 32 x 64 tiles (M <= 32).
 hipError_t launch_splitk_narrow(const GemmOperands& o, GemmParams p, bool out_f32, bool gate, hipStream_t stream);
 hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f32, hipStream_t stream);
+// Activation quantization fused in front of the M <= 32 split-K GEMM, one
+// launch, with the whole quantized activation held in LDS (see
+// gemm_splitk.hip); decode_quant_lds_bytes(M, K) is the LDS it takes.
+struct DecodeQuantArgs {
+  const uint16_t* x;        // bf16 [M x K], row stride ldx elements
+  uint32_t ldx;
+  float* g_enc;             // written (dynamic, by workgroup 0) or read (given G)
+  uint8_t* codes;           // optional outputs ([M x K/2], [M x K/16]), written by workgroup 0
+  uint8_t* scales;
+};
+size_t decode_quant_lds_bytes(int64_t M, int64_t K);
+hipError_t launch_decode_quant_gemm(const GemmOperands& o, GemmParams p, const DecodeQuantArgs& q, bool dynamic,
+                                    bool out_f32, hipStream_t stream);
 // Register path (K % 64 != 0).
 hipError_t launch_reg_square(const GemmOperands& o, GemmParams p, bool out_f32, bool aligned, hipStream_t stream);
 

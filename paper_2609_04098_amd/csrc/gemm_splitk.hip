@@ -17,16 +17,100 @@ namespace nvfp4 {
 // in LDS at the end; fragment f is summed in wave order (deterministic) and
 // stored by wave f % KS.  Requires K % 64 == 0.
 
-template <int KS, int FM, int FN, int kStages, bool kF32Out, bool kGate>
+// Activation quantization fused in front of the split-K GEMM, one launch,
+// for decode shapes whose whole activation fits in LDS (kQuant = 1 with a
+// given G, 2 with the dynamic G).  Every workgroup reads all of X (a few KB
+// to a few tens of KB, from L2 after the first workgroup), takes the global
+// maximum itself in dynamic mode (the maximum is order-free, so every
+// workgroup forms the same G), quantizes every block with the stand-alone
+// quantizer's device code into LDS, and the GEMM then reads its activation
+// fragments from LDS instead of streaming them: one launch, no hand-off
+// between workgroups, and the results of nvfp4_quantize_act + nvfp4_gemm
+// bit for bit (same codes, same summation order).  Workgroup 0 also writes
+// G and, when asked for, the codes and scales.
+
+// Maximum over the workgroup (kThreads threads) of a non-negative value.
+template <int kThreads>
+__device__ __forceinline__ uint32_t wg_max_u32(uint32_t v, uint32_t* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t o = __shfl_xor(v, off, 64);
+    v = v > o ? v : o;
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = red[0];
+#pragma unroll
+  for (int w = 1; w < kThreads / 64; ++w) r = r > red[w] ? r : red[w];
+  __syncthreads();
+  return r;
+}
+
+// The 8 dwords (16 bf16) of block b of X (row-major blocks, bpr per row).
+__device__ __forceinline__ void load_x_block(const DecodeQuantArgs& q, uint32_t b, uint32_t bpr, uint32_t v[8]) {
+  const uint32_t row = b / bpr, col = b - row * bpr;
+  const uint4* src = reinterpret_cast<const uint4*>(q.x + (size_t)row * q.ldx) + 2 * col;
+  const uint4 d0 = src[0], d1 = src[1];
+  v[0] = d0.x; v[1] = d0.y; v[2] = d0.z; v[3] = d0.w;
+  v[4] = d1.x; v[5] = d1.y; v[6] = d1.z; v[7] = d1.w;
+}
+
+// Quantize all of X into the LDS activation (codes [M][K/2], then scales
+// [M][K/16]); returns G.
+template <int kThreads, bool kDynamic>
+__device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p, uint8_t* lds_codes,
+                                   uint8_t* lds_scales, uint32_t* red) {
+  const uint32_t bpr = p.K >> 4, n_blocks = p.M * bpr;
+  float g;
+  if (kDynamic) {
+    uint32_t m = 0;
+    for (uint32_t b = threadIdx.x; b < n_blocks; b += kThreads) {
+      uint32_t v[8];
+      load_x_block(q, b, bpr, v);
+      const uint32_t a = __float_as_uint(block_amax(v));
+      m = m > a ? m : a;                     // non-negative floats order as integers
+    }
+    g = global_scale(__uint_as_float(wg_max_u32<kThreads>(m, red)));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *q.g_enc = g;
+  } else {
+    g = *q.g_enc;
+  }
+  const float gd6 = g * (1.0f / 6.0f);
+  const bool out = q.codes != nullptr && blockIdx.x == 0;
+  for (uint32_t b = threadIdx.x; b < n_blocks; b += kThreads) {
+    uint32_t v[8], c0, c1, sc;
+    load_x_block(q, b, bpr, v);
+    if (g > kHugeScale)
+      sc = quantize_block<true>(v, g, gd6, c0, c1);
+    else
+      sc = quantize_block<false>(v, g, gd6, c0, c1);
+    reinterpret_cast<uint2*>(lds_codes)[b] = make_uint2(c0, c1);
+    lds_scales[b] = (uint8_t)sc;
+    if (out) {
+      reinterpret_cast<uint2*>(q.codes)[b] = make_uint2(c0, c1);
+      q.scales[b] = (uint8_t)sc;
+    }
+  }
+  __syncthreads();
+  return g;
+}
+
+template <int KS, int FM, int FN, int kStages, bool kF32Out, bool kGate, int kQuant = 0>
 __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* __restrict__ a_codes,
                                                              const uint8_t* __restrict__ a_scales,
                                                              const float* __restrict__ a_g,
                                                              const uint8_t* __restrict__ w_packed,
                                                              const float* __restrict__ w_g,
-                                                             void* __restrict__ y, GemmParams p) {
+                                                             void* __restrict__ y, GemmParams p,
+                                                             DecodeQuantArgs q) {
   constexpr int BM = FM * 32, BN = FN * 32;
-  using L = SplitkStage<FM, FN>;
+  // With the fused quantizer the activation sits in LDS and the ring
+  // carries only the weight.
+  constexpr bool kALds = kQuant != 0;
+  static_assert(!kALds || FM == 1, "LDS-resident activation: one 32-row fragment");
+  using L = SplitkStage<kALds ? 0 : FM, FN>;
   constexpr int kFrags = FM + FN;
+  constexpr int kWOff = kALds ? 0 : FM;                      // first weight slot of a stage
   constexpr int kScaleA = L::kScaleA, kScaleB = L::kScaleB, kStageBytes = L::kBytes;
   constexpr int kLoads = L::kLoads;                          // DMA loads per chunk and wave
   constexpr int kWaitFirst = lds::vmcnt_imm((kStages - 1) * kLoads);
@@ -45,7 +129,7 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   // Scale DMA of fragment pair j: lane l loads the scale dword of row l of
   // the pair (A), or of row l % 32 of weight tile l / 32 of the pair (W);
   // the missing second fragment of an odd count reads zeros.
-  uint32_t a_off[FM], as_off[L::kPairsA], b_off[FN], bs_off[L::kPairsB];
+  uint32_t a_off[FM], as_off[L::kPairsA > 0 ? L::kPairsA : 1], b_off[FN], bs_off[L::kPairsB];
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
     const uint32_t row = m0 + f * 32 + r;
@@ -69,9 +153,6 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
   const uint32_t n_mine = wave < p.chunks ? (p.chunks - 1 - wave) / KS + 1 : 0;
-  float alpha[FN];
-  segment_alpha<FN>(p, *a_g, w_g, n0, r, alpha);
-
   const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
   const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
   const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
@@ -79,30 +160,52 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
   // DMA of this wave's i-th chunk into stage i % kStages.  (Prologue loads
   // of chunks past the end of K, when K is short, re-load the last chunk so
   // that every address stays inside its tensor; they are never read.)
-  auto issue = [&](uint32_t i) {
+  auto issue_a = [&](uint32_t i) {
+    if constexpr (!kALds) {
+      const uint32_t kc = wave + KS * i;
+      const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
+      uint8_t* st = ring + (i % kStages) * kStageBytes;
+#pragma unroll
+      for (int f = 0; f < FM; ++f) dma16(ra, st + f * 1024, a_off[f], kq * 32u);
+#pragma unroll
+      for (int j = 0; j < L::kPairsA; ++j) dma4(rs, st + kScaleA + j * 256, as_off[j], kq * 4u);
+    }
+  };
+  auto issue_w = [&](uint32_t i) {
     const uint32_t kc = wave + KS * i;
     const uint32_t kq = kc < p.chunks ? kc : p.chunks - 1;
     uint8_t* st = ring + (i % kStages) * kStageBytes;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) dma16(ra, st + f * 1024, a_off[f], kq * 32u);
-#pragma unroll
-    for (int j = 0; j < L::kPairsA; ++j) dma4(rs, st + kScaleA + j * 256, as_off[j], kq * 4u);
-#pragma unroll
-    for (int f = 0; f < FN; ++f) dma16(rb, st + (FM + f) * 1024, b_off[f], kq * 1024u);
+    for (int f = 0; f < FN; ++f) dma16(rb, st + (kWOff + f) * 1024, b_off[f], kq * 1024u);
 #pragma unroll
     for (int j = 0; j < L::kPairsB; ++j) dma4(rbs, st + kScaleB + j * 256, bs_off[j], kq * 128u);
+  };
+  auto issue = [&](uint32_t i) {
+    issue_a(i);
+    issue_w(i);
   };
 
   struct Regs {
     int4v c[kFrags];
     uint32_t s[kFrags];
   };
+  // LDS-resident activation (fused quantizer): codes [M][K/2], then scales
+  // [M][K/16], after the rings; rows >= M are zero operands.
+  const uint8_t* a_lds = smem + KS * kStages * kStageBytes;
+  const uint8_t* as_lds = a_lds + p.M * (p.K >> 1);
   auto read_stage = [&](Regs& R, uint32_t i) {
     const uint8_t* st = ring + (i % kStages) * kStageBytes;
 #pragma unroll
     for (int f = 0; f < kFrags; ++f) {
-      R.c[f] = *(const int4v*)(st + f * 1024 + lane * 16);
-      R.s[f] = *(const uint32_t*)(st + (f < FM ? kScaleA + f * 128 : kScaleB + (f - FM) * 128) + r * 4);
+      if (kALds && f < FM) {
+        const uint32_t kc = wave + KS * i;
+        const bool live = r < p.M && kc < p.chunks;
+        R.c[f] = live ? *(const int4v*)(a_lds + r * (p.K >> 1) + kc * 32 + h * 16) : int4v{0, 0, 0, 0};
+        R.s[f] = live ? *(const uint32_t*)(as_lds + r * (p.K >> 4) + kc * 4) : 0u;
+      } else {
+        R.c[f] = *(const int4v*)(st + (f - FM + kWOff) * 1024 + lane * 16);
+        R.s[f] = *(const uint32_t*)(st + (f < FM ? kScaleA + f * 128 : kScaleB + (f - FM) * 128) + r * 4);
+      }
     }
   };
 
@@ -164,9 +267,23 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
     }
   };
 
+  float alpha[FN];
+  if constexpr (kQuant != 0) {
+    // The weight's first stages do not depend on the activation: their
+    // loads fly while the workgroup quantizes X into LDS.
+    __shared__ uint32_t red[KS];
 #pragma unroll
-  for (int s = 0; s < kStages; ++s) issue(s);
-  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+    for (int s = 0; s < kStages; ++s) issue_w(s);
+    uint8_t* a_dst = smem + KS * kStages * kStageBytes;
+    const float ga = quantize_into_lds<KS * 64, kQuant == 2>(q, p, a_dst, a_dst + p.M * (p.K >> 1), red);
+    segment_alpha<FN>(p, ga, w_g, n0, r, alpha);
+    __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  } else {
+    segment_alpha<FN>(p, *a_g, w_g, n0, r, alpha);
+#pragma unroll
+    for (int s = 0; s < kStages; ++s) issue(s);
+    __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  }
   Regs cur, nxt;
   read_stage(cur, 0);
   for (uint32_t i = 0; i < n_mine; ++i) {
@@ -195,7 +312,7 @@ static hipError_t launch_splitk(const GemmOperands& o, GemmParams p, bool out_f3
   const dim3 grid(p.tiles_m * p.tiles_n), block(KS * 64);
 #define NVFP4_SK(F32, GATE)                                                                           \
   hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, F32, GATE>), grid, block, kLds, stream, \
-                     o.a_codes, o.a_scales, o.a_g, o.w_packed, o.w_g, o.y, p)
+                     o.a_codes, o.a_scales, o.a_g, o.w_packed, o.w_g, o.y, p, DecodeQuantArgs{})
   if (gate) {
     if (out_f32) NVFP4_SK(true, true); else NVFP4_SK(false, true);
   } else {
@@ -211,6 +328,31 @@ hipError_t launch_splitk_narrow(const GemmOperands& o, GemmParams p, bool out_f3
 
 hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f32, hipStream_t stream) {
   return launch_splitk<4, 1, 2, 3>(o, p, out_f32, false, stream);
+}
+
+size_t decode_quant_lds_bytes(int64_t M, int64_t K) {
+  return (size_t)(4 * 3 * SplitkStage<0, 2>::kBytes) + (size_t)(M * K / 2 + M * K / 16);
+}
+
+hipError_t launch_decode_quant_gemm(const GemmOperands& o, GemmParams p, const DecodeQuantArgs& q, bool dynamic,
+                                    bool out_f32, hipStream_t stream) {
+  constexpr int KS = 4, FM = 1, FN = 2, kStages = 3;
+  constexpr int kRing = KS * kStages * SplitkStage<0, FN>::kBytes;
+  static_assert(kRing >= KS * 64 * 64, "the reduction reuses the rings");
+  const size_t lds = decode_quant_lds_bytes(p.M, p.K);
+  p.tiles_m = 1;
+  p.tiles_n = (p.N + FN * 32 - 1) / (FN * 32);
+  const dim3 grid(p.tiles_n), block(KS * 64);
+#define NVFP4_DQ(F32, Q)                                                                                   \
+  hipLaunchKernelGGL((gemm_splitk_kernel<KS, FM, FN, kStages, F32, false, Q>), grid, block, (uint32_t)lds, stream, \
+                     o.a_codes, o.a_scales, o.a_g, o.w_packed, o.w_g, o.y, p, q)
+  if (dynamic) {
+    if (out_f32) NVFP4_DQ(true, 2); else NVFP4_DQ(false, 2);
+  } else {
+    if (out_f32) NVFP4_DQ(true, 1); else NVFP4_DQ(false, 1);
+  }
+#undef NVFP4_DQ
+  return hipGetLastError();
 }
 
 }  // namespace nvfp4

@@ -62,8 +62,11 @@ hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales
                                  const float* a_log, const float* dt_bias, void* y, int64_t ldy,
                                  bool out_f32, hipStream_t stream);
 
+// nvfp4_quantize_gemm: M <= 32 with N > 128 takes the fused decode path.
+bool quant_gemm_uses_decode_path(int64_t M, int64_t N);
+size_t quant_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* g_enc, bool dynamic,
-                             float* partial, const void* w_packed, int64_t N, const int64_t* seg_offsets,
+                             void* workspace, const void* w_packed, int64_t N, const int64_t* seg_offsets,
                              int n_seg, const float* w_g, uint8_t* codes, uint8_t* scales, void* y, int64_t ldy,
                              bool out_f32, hipStream_t stream);
 

@@ -1,5 +1,6 @@
-// Activation quantization fused into the narrow NVFP4 GEMM
-// (nvfp4_quantize_gemm).
+// Activation quantization fused into the NVFP4 GEMM (nvfp4_quantize_gemm):
+// the narrow-output kernel below (N <= 128), and the host side of the fused
+// decode path (M <= 32, the split-K kernel's fused prologue).
 #include "gemm_common.h"
 
 namespace nvfp4 {
@@ -199,13 +200,58 @@ static hipError_t launch_quant_gemm_fn(const QuantGemmArgs& q, bool dynamic, con
   return hipGetLastError();
 }
 
+namespace {
+
+size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
+
+// The fused decode kernel quantizes all of X in every workgroup (there is
+// no hand-off between workgroups), so it pays off only while X is a few
+// tokens: up to M * K = 16384 elements (3 tokens of width 5120) it beats
+// the quantizer launch in front of the GEMM (1 token: 33.0 vs 34.5 us on
+// the gate/up weight read from HBM); at 7 tokens the repeated quantization
+// already costs more than the launch (43.6 vs 36.7 us).
+constexpr int64_t kDecodeFuseMaxElems = 16384;
+
+}  // namespace
+
+bool quant_gemm_uses_decode_path(int64_t M, int64_t N) { return M >= 1 && M <= 32 && N > 128; }
+
+// Workspace of nvfp4_quantize_gemm: the partial maxima of the amax pass
+// (kActScratchBytes); on the decode path also room for the quantized
+// activation (codes, then scales) when it runs as two launches.
+size_t quant_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  size_t bytes = kActScratchBytes;
+  if (quant_gemm_uses_decode_path(M, N)) bytes += align16((size_t)(M * K / 2)) + align16((size_t)(M * K / 16));
+  return bytes;
+}
+
 hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, float* g_enc, bool dynamic,
-                             float* partial, const void* w_packed, int64_t N, const int64_t* seg_offsets,
+                             void* workspace, const void* w_packed, int64_t N, const int64_t* seg_offsets,
                              int n_seg, const float* w_g, uint8_t* codes, uint8_t* scales, void* y, int64_t ldy,
                              bool out_f32, hipStream_t stream) {
+  float* partial = static_cast<float*>(workspace);
   if (M == 0) {   // G as the quantizer writes it for an empty tensor
     if (!dynamic) return hipSuccess;
     return launch_act_quant(x, 0, K, ldx, codes, scales, g_enc, true, partial, stream);
+  }
+  GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
+  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
+  if (quant_gemm_uses_decode_path(M, N)) {
+    if (M * K <= kDecodeFuseMaxElems) {
+      // One launch: every workgroup quantizes X into its LDS.
+      const DecodeQuantArgs dq{static_cast<const uint16_t*>(x), (uint32_t)ldx, g_enc, codes, scales};
+      const GemmOperands o{codes, scales, g_enc, wp, w_g, y};
+      return launch_decode_quant_gemm(o, p, dq, dynamic, out_f32, stream);
+    }
+    // Larger activations: the quantizer, then the same GEMM kernel reading
+    // the codes from memory (the caller's buffers or the workspace).
+    uint8_t* ws = static_cast<uint8_t*>(workspace) + kActScratchBytes;
+    uint8_t* a_codes = codes != nullptr ? codes : ws;
+    uint8_t* a_scales = scales != nullptr ? scales : ws + align16((size_t)(M * K / 2));
+    hipError_t e = launch_act_quant(x, M, K, ldx, a_codes, a_scales, g_enc, dynamic, partial, stream);
+    if (e != hipSuccess) return e;
+    const GemmOperands o{a_codes, a_scales, g_enc, wp, w_g, y};
+    return launch_splitk_decode(o, p, out_f32, stream);
   }
   QuantGemmArgs q{};
   q.x = static_cast<const uint16_t*>(x);
@@ -221,8 +267,6 @@ hipError_t launch_quant_gemm(const void* x, int64_t M, int64_t K, int64_t ldx, f
     if (e != hipSuccess) return e;
     q.n_partial = (uint32_t)n_partial;
   }
-  GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
-  const uint8_t* wp = static_cast<const uint8_t*>(w_packed);
   if (N <= 96) return launch_quant_gemm_fn<4, 2, 3, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
   return launch_quant_gemm_fn<4, 1, 4, 1>(q, dynamic, wp, w_g, y, p, out_f32, stream);
 }

@@ -137,9 +137,13 @@ def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype
     return y
 
 
+def quantize_gemm_workspace(m, n, k, device):
+    return torch.empty(_c.nvfp4_quantize_gemm_workspace(m, n, k), dtype=torch.uint8, device=device)
+
+
 def quantize_gemm(x, pw: PackedWeight, g=None, out_dtype=torch.bfloat16, out=None, act_out: QuantizedAct = None,
                   workspace=None, stream=None):
-    """Act-quant fused into a narrow GEMM (N <= 128): y [M, N] equal to
+    """Act-quant fused into the GEMM (N <= 128, or M <= 32): y [M, N] equal to
     gemm(quantize_act(x, g), pw).  Dynamic G unless ``g`` is given; the
     activation codes/scales/G are written to ``act_out`` when it is given.
     Returns (y, G as a device float32 [1])."""
@@ -152,13 +156,13 @@ def quantize_gemm(x, pw: PackedWeight, g=None, out_dtype=torch.bfloat16, out=Non
     gbuf = act_out.g if act_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
     codes = act_out.codes if act_out is not None else None
     scales = act_out.scales if act_out is not None else None
+    ws = quantize_gemm_workspace(m, pw.n, k, dev) if workspace is None else workspace
     if g is None:
-        ws = act_workspace(m, k, dev) if workspace is None else workspace
         _c.nvfp4_quantize_gemm(x, gbuf, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, _c.NVFP4_DYNAMIC, ws,
                                codes, scales, kind, stream)
     else:
         gbuf.copy_(torch.as_tensor([float(g)], dtype=torch.float32))
-        _c.nvfp4_quantize_gemm(x, gbuf, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, _c.NVFP4_STATIC, None,
+        _c.nvfp4_quantize_gemm(x, gbuf, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, _c.NVFP4_STATIC, ws,
                                codes, scales, kind, stream)
     return y, gbuf
 

@@ -46,6 +46,7 @@ SIGNATURES = {
                                     _c_int64, _int, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
                           _c_int64, _int, _vp]),
+    "nvfp4_quantize_gemm_workspace": (_sz, [_c_int64, _c_int64, _c_int64]),
     "nvfp4_quantize_gemm": (_int, [_vp, _c_int64, _c_int64, _c_int64, _vp, _int, _vp, _sz, _vp, _c_int64,
                                    _vp, _int, _vp, _vp, _vp, _vp, _c_int64, _int, _vp]),
 }
@@ -202,9 +203,14 @@ def nvfp4_gemm_gdn_gates(a_codes, a_scales, a_g_enc, w_packed, H, w_g_enc_seg, a
     _check(st, "nvfp4_gemm_gdn_gates")
 
 
+def nvfp4_quantize_gemm_workspace(M, N, K):
+    return lib().nvfp4_quantize_gemm_workspace(int(M), int(N), int(K))
+
+
 def nvfp4_quantize_gemm(x, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y, mode=NVFP4_DYNAMIC,
                         workspace=None, a_codes=None, a_scales=None, y_dtype=NVFP4_BF16, stream=None):
-    """Y [M, N] = quantize(x) then the segment-scaled GEMM, fused (N <= 128);
+    """Y [M, N] = quantize(x) then the segment-scaled GEMM, fused (N <= 128 or
+    M <= 32);
     x bf16 [M, K] (row stride x.stride(0)); optional a_codes / a_scales
     outputs."""
     M, K = x.shape

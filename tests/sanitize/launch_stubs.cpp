@@ -39,7 +39,11 @@ hipError_t launch_gemm_gdn_gates(const uint8_t*, const uint8_t*, const float*, i
                                  const float*, const float*, const float*, void*, int64_t, bool, hipStream_t) {
   return hipErrorNoDevice;
 }
-hipError_t launch_quant_gemm(const void*, int64_t, int64_t, int64_t, float*, bool, float*, const void*, int64_t,
+bool quant_gemm_uses_decode_path(int64_t M, int64_t N) { return M >= 1 && M <= 32 && N > 128; }
+size_t quant_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  return 4096 + (quant_gemm_uses_decode_path(M, N) ? (size_t)(M * K) : 0);
+}
+hipError_t launch_quant_gemm(const void*, int64_t, int64_t, int64_t, float*, bool, void*, const void*, int64_t,
                              const int64_t*, int, const float*, uint8_t*, uint8_t*, void*, int64_t, bool,
                              hipStream_t) {
   return hipErrorNoDevice;

@@ -206,7 +206,12 @@ def test_quantize_gemm_rejects_bad_arguments():
     assert call(y=FAKE + 1) == C.NVFP4_EINVAL
     assert call(mode=C.NVFP4_DYNAMIC) == C.NVFP4_EINVAL          # no workspace
     assert call(mode=C.NVFP4_DYNAMIC, ws=FAKE, wsb=4) == C.NVFP4_EWORKSPACE
-    assert call(N=160, segs=_offs([0, 160]), nseg=1, ldy=160) == C.NVFP4_EUNSUPPORTED   # N > 128
+    assert call(M=33, N=160, segs=_offs([0, 160]), nseg=1, ldy=160) == C.NVFP4_EUNSUPPORTED   # N > 128, M > 32
+    # M <= 32 with N > 128 (the decode path) needs a workspace in both modes
+    assert call(M=32, N=160, segs=_offs([0, 160]), nseg=1, ldy=160) == C.NVFP4_EINVAL
+    wsb = C.lib().nvfp4_quantize_gemm_workspace(32, 160, 128)
+    assert wsb >= 4096 + 32 * 128 // 2 + 32 * 128 // 16
+    assert call(M=32, N=160, segs=_offs([0, 160]), nseg=1, ldy=160, ws=FAKE, wsb=wsb - 1) == C.NVFP4_EWORKSPACE
     assert call(K=80, ldx=80) == C.NVFP4_EUNSUPPORTED             # K % 64 != 0
 
 

@@ -116,3 +116,75 @@ def test_quantize_gemm_full_ab_gates():
     args = (wl["xp"], wl["xs"], wl["gx"], wl["wp"], wl["ws"], wl["gw"], cfg.seg_offsets)
     check_gemm(y32[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64),
                OG.gemm_f64(*args, rows=rows), OG.abs_bound(*args, rows=rows), "ab_gates fused")
+
+
+# ---------------------------------------------------------------- decode path
+# M <= 32 with N > 128: one launch in which every workgroup quantizes X into
+# its LDS and runs the M <= 32 split-K GEMM on it (activations up to 24 KB
+# quantized), else the quantizer and the same GEMM; Y must equal the unfused
+# quantize + GEMM bit for bit either way.
+
+@pytest.mark.parametrize("m,n,k,offs", [
+    (1, 300, 1024, [0, 300]),              # one row, ragged N
+    (7, 520, 5120, [0, 260, 520]),         # hidden width, two segments
+    (32, 200, 128, [0, 72, 200]),          # 2 chunks < 4 waves
+    (17, 4100, 256, [0, 4000, 4100]),      # many workgroups, few blocks each
+    (5, 129, 64, [0, 129]),                # one chunk, N just past the narrow limit
+    (20, 300, 2560, [0, 150, 300]),        # 28.8 KB quantized: the two-launch decode path
+])
+def test_quantize_gemm_decode_matches_unfused(m, n, k, offs):
+    rng = np.random.default_rng(m * 11 + n * 7 + k)
+    x, w = _xw(rng, m, n, k)
+    check_case(x, w, offs)                                  # dynamic G
+    check_case(x, w, offs, g=np.float32(2688.0 / 40.0))    # static G, saturating outliers
+    check_case(x, w, offs, ldx=k + 64)                      # strided rows
+
+
+def test_quantize_gemm_decode_edge_values():
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((9, 256))
+    x[0] = 0.0
+    x[1, :16] = 0.0
+    x[2, :16] *= 1e-4
+    x[2, 16] = 3e3
+    xb = bits_of(x)
+    xb[3, ::3] = 0x8000
+    w = bits_of(rng.standard_normal((160, 256)) * 0.05)
+    check_case(xb, w, [0, 100, 160])
+    check_case(xb, w, [0, 100, 160], g=np.float32(3e30))
+    check_case(np.zeros((4, 256), dtype=np.uint16), w, [0, 100, 160])
+
+
+@pytest.mark.parametrize("m", [1, 7, 32])
+def test_quantize_gemm_decode_full_gate_up(m):
+    """Decode rows against the full gate/up weight (34816 x 5120, two
+    segments): codes, scales and G equal the oracle's, Y equals the unfused
+    path bit for bit and the oracle within the GEMM tolerance on every
+    element; three calls on one workspace agree."""
+    wl = workload("decode_m32")
+    cfg = wl["cfg"]
+    x_bits = wl["x"][:m]
+    x = to_dev_bf16(x_bits)
+    pw = L.pack_weight(to_dev_bf16(wl["w"]), cfg.seg_offsets)
+    log("decode m=%d: fused quantize + GEMM on GPU" % m)
+    aq_ref = L.quantize_act(x)
+    y_ref = L.gemm(aq_ref, pw, out_dtype=torch.float32)
+    ws = L.quantize_gemm_workspace(m, cfg.n, cfg.k, x.device)
+    aq = L.alloc_act(m, cfg.k, x.device)
+    ys = []
+    for i in range(3):
+        y32, g32 = L.quantize_gemm(x, pw, out_dtype=torch.float32, act_out=aq if i == 0 else None, workspace=ws)
+        ys.append(y32)
+    y16, _ = L.quantize_gemm(x, pw, out_dtype=torch.bfloat16, workspace=ws)
+    torch.cuda.synchronize()
+    xp, xs, gx = OQ.quantize_tensor(x_bits)
+    assert np.float32(g32.item()) == gx == np.float32(aq.g.item())
+    np.testing.assert_array_equal(np_u8(aq.codes), xp)
+    np.testing.assert_array_equal(np_u8(aq.scales), xs)
+    for y32 in ys:
+        assert torch.equal(y32, y_ref), "fused decode GEMM differs from the unfused path"
+    assert torch.equal(y16.view(torch.int16), ys[0].to(torch.bfloat16).view(torch.int16))
+    args = (xp, xs, gx, wl["wp"], wl["ws"], wl["gw"], cfg.seg_offsets)
+    rel = check_gemm(ys[0].cpu().numpy().astype(np.float64), OG.gemm_f64(*args), OG.abs_bound(*args),
+                     "decode m=%d" % m)
+    log("decode m=%d: relative Frobenius error %.3g" % (m, rel))
