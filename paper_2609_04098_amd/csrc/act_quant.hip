@@ -96,7 +96,11 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* 
 }
 
 // Grid-strided loop over 16-element blocks: 32 bytes of bf16 in, 8 bytes of
-// packed codes and 1 scale byte out per block.
+// packed codes and 1 scale byte out per block.  The next block's loads are
+// issued before the current block is quantized (two blocks in flight per
+// thread).  (Walking the blocks from the end of X to its start after the
+// amax pass, so as to meet the most recently read part of X in the MALL,
+// measured 2% slower on a 335 MB activation and is not done.)
 template <bool kContig, bool kHuge>
 __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, uint32_t n_blocks,
                                                 uint32_t blocks_per_row, uint32_t ldx,
@@ -104,20 +108,30 @@ __device__ __forceinline__ void quantize_blocks(const uint16_t* __restrict__ x, 
                                                 float g) {
   const float gd6 = g * (1.0f / 6.0f);
   const uint32_t stride = gridDim.x * kThreads;
-  for (uint32_t b = blockIdx.x * kThreads + threadIdx.x; b < n_blocks; b += stride) {
-    const uint4* src;
-    if (kContig) {
-      src = reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
-    } else {
-      uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
-      src = reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+  auto src_of = [&](uint32_t b) -> const uint4* {
+    if (kContig) return reinterpret_cast<const uint4*>(x) + 2 * (size_t)b;
+    const uint32_t row = b / blocks_per_row, col = b - row * blocks_per_row;
+    return reinterpret_cast<const uint4*>(x + (size_t)row * ldx) + 2 * col;
+  };
+  uint32_t i = blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n_blocks) return;
+  const uint4* src = src_of(i);
+  uint4 d0 = src[0], d1 = src[1];
+  for (; i < n_blocks; i += stride) {
+    const uint32_t b = i;
+    uint4 e0 = d0, e1 = d1;
+    if (i + stride < n_blocks) {
+      const uint4* nxt = src_of(i + stride);
+      e0 = nxt[0];
+      e1 = nxt[1];
     }
-    uint4 d0 = src[0], d1 = src[1];
-    uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    const uint32_t v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
     uint32_t c0, c1;
-    uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
+    const uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
     reinterpret_cast<uint2*>(codes)[b] = make_uint2(c0, c1);
     scales[b] = (uint8_t)sc;
+    d0 = e0;
+    d1 = e1;
   }
 }
 

@@ -15,8 +15,11 @@ constexpr int kActPartials = 1024;
 // Bytes of the per-device scratch array of the allocation-free quantizer
 // (the partial maxima).
 constexpr size_t kActScratchBytes = kActPartials * sizeof(float);
-// Upper bound on quantize workgroups (grid-strided beyond that).
-constexpr int kActQuantGridCap = 4096;
+// Upper bound on quantize workgroups (grid-strided beyond that): 8 per CU
+// of a 256-CU device, 8 waves per SIMD.  In dynamic mode every workgroup
+// first reduces the amax pass's partial maxima, so fewer, longer-lived
+// workgroups spend less on that preamble.
+constexpr int kActQuantGridCap = 2048;
 // Partial maxima per weight segment.
 constexpr int kWeightPartials = 256;
 

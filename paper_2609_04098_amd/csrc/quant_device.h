@@ -72,29 +72,74 @@ __device__ __forceinline__ float block_amax(const uint32_t v[8]) {
   return __uint_as_float(mx << 16);
 }
 
-// E4M3 code of RNE_E4M3(amax_b * G / 6), exactly.  gd6 is any approximation
-// of G / 6 within a few ulps.
-__device__ __forceinline__ uint32_t scale_code(float amax_b, float g, float gd6) {
-  float ua = amax_b * gd6;                           // ~ amax_b G / 6
-  // Nearest point of the lattice {E4M3 values and midpoints}: multiples of
-  // 2^(e-4) in binade [2^e, 2^(e+1)) for e >= -6, multiples of 2^-10 below.
-  float l_norm = __uint_as_float((__float_as_uint(ua) + 0x40000u) & 0xFFF80000u);
-  float l_sub = __builtin_rintf(ua * 1024.0f) * 0x1p-10f;
-  float l = ua >= 0x1p-6f ? l_norm : l_sub;
-  int s = sign3(__builtin_fmaf(amax_b, g, -6.0f * l)); // sign(amax_b G - 6 L)
-  float w = __uint_as_float(__float_as_uint(l) + (uint32_t)s);
-  // RNE of w onto E4M3 (w >= 0): subnormal range by rint, else round the
-  // binary32 significand to 3 bits; saturate to 448 (code 126).
-  uint32_t code_sub = (uint32_t)__builtin_rintf(w * 512.0f);
-  uint32_t b = __float_as_uint(w);
-  uint32_t code_norm = ((b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20) - 960u;
-  code_norm = code_norm < 126u ? code_norm : 126u;
-  return w < 0x1p-6f ? code_sub : code_norm;
-}
-
 // Value of an E4M3 scale code (OCP E4M3FN; the hardware conversion).
 __device__ __forceinline__ float scale_value(uint32_t code) {
   return __builtin_amdgcn_cvt_f32_fp8((int)code, 0);
+}
+
+// Block scale S = RNE_E4M3(amax_b * G / 6), exactly, as its E4M3 code and
+// its value, with rq4 ~ 4 / S (0 when S = 0).  gd6 is any approximation of
+// G / 6 within a few ulps; ua = amax_b * gd6 approximates amax_b G / 6.
+//
+// Normal scales (ua >= 2^-6, every block but nearly-empty ones): the lattice
+// of E4M3 values and midpoints is the multiples of 2^(e-4) in binade
+// [2^e, 2^(e+1)); the nudged lattice point w is rounded by keeping 3
+// significand bits, saturating at 448 (code 126).  (w can fall just below
+// 2^-6 only when the exact value does; it then rounds to code 8 = 2^-6,
+// as it must.)
+// Subnormal range (ua < 2^-6): the lattice is the multiples of 2^-10 and the
+// code is rint(w * 2^9) (up to 8 = 2^-6).  The branch is rarely taken: when
+// no lane of a wave takes it, it costs nothing.
+struct BlockScale {
+  uint32_t code;
+  float s;      // S, exact
+  float rq4;    // ~ 4 / S (0 when S = 0)
+};
+
+// kBranch = false evaluates both ranges and selects (no branch: for callers
+// whose register budget is tight, where the branch's extra live values
+// would spill); the results are identical.
+template <bool kBranch = true>
+__device__ __forceinline__ BlockScale block_scale(float amax_b, float g, float gd6) {
+  const float ua = amax_b * gd6;
+  BlockScale r;
+  if (!kBranch) {
+    const float l_norm = __uint_as_float((__float_as_uint(ua) + 0x40000u) & 0xFFF80000u);
+    const float l_sub = __builtin_rintf(ua * 1024.0f) * 0x1p-10f;
+    const float l = ua >= 0x1p-6f ? l_norm : l_sub;
+    const int sg = sign3(__builtin_fmaf(amax_b, g, -6.0f * l));
+    const float w = __uint_as_float(__float_as_uint(l) + (uint32_t)sg);
+    const uint32_t code_sub = (uint32_t)__builtin_rintf(w * 512.0f);
+    const uint32_t b = __float_as_uint(w);
+    uint32_t code_norm = ((b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20) - 960u;
+    code_norm = code_norm < 126u ? code_norm : 126u;
+    r.code = w < 0x1p-6f ? code_sub : code_norm;
+    r.s = scale_value(r.code);
+    r.rq4 = r.s > 0.0f ? 4.0f * __builtin_amdgcn_rcpf(r.s) : 0.0f;
+    return r;
+  }
+  if (ua >= 0x1p-6f) {
+    const float l = __uint_as_float((__float_as_uint(ua) + 0x40000u) & 0xFFF80000u);
+    const int sg = sign3(__builtin_fmaf(amax_b, g, -6.0f * l));    // sign(amax_b G - 6 L)
+    const uint32_t b = __float_as_uint(l) + (uint32_t)sg;
+    const uint32_t code = ((b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20) - 960u;
+    r.code = code < 126u ? code : 126u;
+    r.s = scale_value(r.code);
+    r.rq4 = 4.0f * __builtin_amdgcn_rcpf(r.s);
+  } else {
+    const float l = __builtin_rintf(ua * 1024.0f) * 0x1p-10f;
+    const int sg = sign3(__builtin_fmaf(amax_b, g, -6.0f * l));
+    const float w = __uint_as_float(__float_as_uint(l) + (uint32_t)sg);
+    r.code = (uint32_t)__builtin_rintf(w * 512.0f);
+    r.s = scale_value(r.code);
+    r.rq4 = r.s > 0.0f ? 4.0f * __builtin_amdgcn_rcpf(r.s) : 0.0f;
+  }
+  return r;
+}
+
+// E4M3 code of RNE_E4M3(amax_b * G / 6), exactly (see block_scale).
+__device__ __forceinline__ uint32_t scale_code(float amax_b, float g, float gd6) {
+  return block_scale(amax_b, g, gd6).code;
 }
 
 struct ElemConsts {
@@ -109,11 +154,11 @@ struct ElemConsts {
 // is uniform across a launch.
 constexpr float kHugeScale = 0x1p100f;
 
-__device__ __forceinline__ ElemConsts elem_consts(float g, float s) {
+__device__ __forceinline__ ElemConsts elem_consts(float g, const BlockScale& bs) {
   ElemConsts c;
   c.g = g;
-  c.sq = s * 0.25f;
-  c.rq4 = s > 0.0f ? 4.0f * __builtin_amdgcn_rcpf(s) : 0.0f;
+  c.sq = bs.s * 0.25f;
+  c.rq4 = bs.rq4;
   c.grq = g * c.rq4;
   return c;
 }
@@ -157,7 +202,7 @@ __device__ __forceinline__ uint32_t encode8(const float* f, const ElemConsts& k)
 // returns the E4M3 scale code.  The block maximum is taken on the widened
 // values (|.| is a free source modifier of the three-input maximum); it is
 // exact, bf16 values being binary32 values, subnormals included.
-template <bool kHuge>
+template <bool kHuge, bool kBranch = true>
 __device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g, float gd6,
                                                    uint32_t& c0, uint32_t& c1) {
   float f[16];
@@ -170,11 +215,11 @@ __device__ __forceinline__ uint32_t quantize_block(const uint32_t v[8], float g,
 #pragma unroll
   for (int i = 3; i < 15; i += 2) amax_b = max3_abs(amax_b, f[i], f[i + 1]);
   amax_b = max3_abs(amax_b, f[15], f[15]);
-  uint32_t sc = scale_code(amax_b, g, gd6);
-  ElemConsts k = elem_consts(g, scale_value(sc));
+  const BlockScale bs = block_scale<kBranch>(amax_b, g, gd6);
+  const ElemConsts k = elem_consts(g, bs);
   c0 = encode8<kHuge>(f, k);
   c1 = encode8<kHuge>(f + 8, k);
-  return sc;
+  return bs.code;
 }
 
 }  // namespace nvfp4

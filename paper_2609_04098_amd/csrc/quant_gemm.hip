@@ -67,12 +67,16 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
   // Per-lane offsets; the chunk goes in the scalar offset.  Rows >= M read
   // zeros (an all-zero block quantizes to zero codes and is not stored).
   const __amdgpu_buffer_rsrc_t rx = rsrc(q.x, q.x_bytes);
-  uint32_t x_off[FM];
+  uint32_t x_off[FM], c_off[FM], s_off[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
     const uint32_t row = m0 + f * 32 + r;
     x_off[f] = row < p.M ? row * q.ldx_bytes + h * 64u : kOOB;
+    c_off[f] = row < p.M ? row * (p.K >> 1) + h * 16u : kOOB;
+    s_off[f] = row < p.M ? row * (p.K >> 4) + h * 2u : kOOB;
   }
+  const __amdgpu_buffer_rsrc_t rc = rsrc(q.codes, p.a_code_bytes);
+  const __amdgpu_buffer_rsrc_t rsc = rsrc(q.scales, p.a_scale_bytes);
   uint32_t b_off[FN], bs_off[FN];
 #pragma unroll
   for (int f = 0; f < FN; ++f) {
@@ -124,14 +128,14 @@ __global__ __launch_bounds__(KS * 64, 2) void quant_gemm_kernel(QuantGemmArgs q,
         const uint32_t v1[8] = {(uint32_t)c.x[f][2][0], (uint32_t)c.x[f][2][1], (uint32_t)c.x[f][2][2],
                                 (uint32_t)c.x[f][2][3], (uint32_t)c.x[f][3][0], (uint32_t)c.x[f][3][1],
                                 (uint32_t)c.x[f][3][2], (uint32_t)c.x[f][3][3]};
-        const uint32_t s0 = quantize_block<kHuge>(v0, g, gd6, cd[f][0], cd[f][1]);
-        const uint32_t s1 = quantize_block<kHuge>(v1, g, gd6, cd[f][2], cd[f][3]);
-        const uint32_t row = m0 + f * 32 + r;
-        if (kCodes && row < p.M) {
-          *reinterpret_cast<uint4*>(q.codes + (size_t)row * (p.K >> 1) + kc * 32u + h * 16u) =
-              make_uint4(cd[f][0], cd[f][1], cd[f][2], cd[f][3]);
-          *reinterpret_cast<uint16_t*>(q.scales + (size_t)row * (p.K >> 4) + kc * 4u + h * 2u) =
-              (uint16_t)(s0 | (s1 << 8));
+        const uint32_t s0 = quantize_block<kHuge, false>(v0, g, gd6, cd[f][0], cd[f][1]);
+        const uint32_t s1 = quantize_block<kHuge, false>(v1, g, gd6, cd[f][2], cd[f][3]);
+        if (kCodes) {
+          // Buffer stores: the lane's offset is fixed, the chunk goes in the
+          // scalar offset; rows >= M have offsets past the buffers (dropped).
+          __builtin_amdgcn_raw_buffer_store_b128(int4v{(int)cd[f][0], (int)cd[f][1], (int)cd[f][2], (int)cd[f][3]},
+                                                 rc, c_off[f], kc * 32u, 0);
+          __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(s0 | (s1 << 8)), rsc, s_off[f], kc * 4u, 0);
         }
         sa[f] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s0 | (s1 << 8), 1.0f, false);
       }
