@@ -37,8 +37,11 @@ MFMA_F16_PEAK_TFLOPS = 2500.0      # MI355X dense FP16/BF16 MFMA
 MXFP4_PEAK_TFLOPS = 10100.0        # MI355X dense FP4 MFMA (reported for context)
 HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
 WORKLOAD = "mlp_gate_up"
-GEMM_SOURCES = ["paper_2609_04098_amd/csrc/gemm.hip", "paper_2609_04098_amd/csrc/packed_layout.h",
-                "paper_2609_04098_amd/csrc/launch.h"]
+# Sources of the headline GEMM kernel (gemm_lds_kernel<LdsSquareSuper>); the
+# committed HBM byte counters are used only while their hash matches.
+GEMM_SOURCES = ["paper_2609_04098_amd/csrc/gemm.hip", "paper_2609_04098_amd/csrc/gemm_common.h",
+                "paper_2609_04098_amd/csrc/gemm_lds.h", "paper_2609_04098_amd/csrc/gemm_lds_super.hip",
+                "paper_2609_04098_amd/csrc/packed_layout.h", "paper_2609_04098_amd/csrc/launch.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_mlp_gate_up_traffic.md")
 
 

@@ -13,12 +13,15 @@
 // squares in binary32: lane l accumulates its blocks l, l + 64, ... in order,
 // two exact squares per v_dot2_f32_bf16, then a butterfly over the 64 lanes
 // (every lane ends with the same value).  r uses correctly rounded division
-// and square root.  Pass 2 re-reads the row (now in the caches), normalizes,
+// and square root.  Pass 2 (from the registers of pass 1 for rows of up to
+// 8192 elements, else a re-read of the row) normalizes,
 // rounds each value to bf16 with the hardware conversion (round to nearest
 // even) and quantizes 16-element blocks exactly as the stand-alone quantizer
 // does.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "launch.h"
 #include "quant_device.h"
@@ -33,30 +36,27 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, (bf16x2){(__bf16)lo, (__bf16)hi});
 }
 
+// Normalize, round to bf16 and quantize block b of one row (d0, d1: its
+// 16 bf16 values).
 template <bool kHuge>
-__device__ __forceinline__ void norm_quant_row(const uint4* __restrict__ xr, const uint4* __restrict__ gr,
-                                               uint32_t nb, float r, float g, uint2* __restrict__ codes_row,
-                                               uint8_t* __restrict__ scales_row, uint4* __restrict__ y_row,
-                                               uint32_t lane) {
-  const float gd6 = g * (1.0f / 6.0f);
-  for (uint32_t b = lane; b < nb; b += 64) {
-    const uint4 d0 = xr[2 * b], d1 = xr[2 * b + 1];
-    const uint4 e0 = gr[2 * b], e1 = gr[2 * b + 1];
-    const uint32_t xv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-    const uint32_t gv[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
-    uint32_t v[8];
+__device__ __forceinline__ void norm_quant_block(uint4 d0, uint4 d1, uint32_t b, const uint4* __restrict__ gr,
+                                                 float r, float g, float gd6, uint2* __restrict__ codes_row,
+                                                 uint8_t* __restrict__ scales_row, uint4* __restrict__ y_row) {
+  const uint4 e0 = gr[2 * b], e1 = gr[2 * b + 1];
+  const uint32_t xv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+  const uint32_t gv[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+  uint32_t v[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      v[i] = pack_bf16((bf16_lo(xv[i]) * r) * bf16_lo(gv[i]), (bf16_hi(xv[i]) * r) * bf16_hi(gv[i]));
-    if (y_row != nullptr) {
-      y_row[2 * b] = make_uint4(v[0], v[1], v[2], v[3]);
-      y_row[2 * b + 1] = make_uint4(v[4], v[5], v[6], v[7]);
-    }
-    uint32_t c0, c1;
-    const uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
-    codes_row[b] = make_uint2(c0, c1);
-    scales_row[b] = (uint8_t)sc;
+  for (int i = 0; i < 8; ++i)
+    v[i] = pack_bf16((bf16_lo(xv[i]) * r) * bf16_lo(gv[i]), (bf16_hi(xv[i]) * r) * bf16_hi(gv[i]));
+  if (y_row != nullptr) {
+    y_row[2 * b] = make_uint4(v[0], v[1], v[2], v[3]);
+    y_row[2 * b + 1] = make_uint4(v[4], v[5], v[6], v[7]);
   }
+  uint32_t c0, c1;
+  const uint32_t sc = quantize_block<kHuge>(v, g, gd6, c0, c1);
+  codes_row[b] = make_uint2(c0, c1);
+  scales_row[b] = (uint8_t)sc;
 }
 
 // Sum of x^2 over the lane's blocks lane, lane + 64, ... in that order, two
@@ -72,8 +72,11 @@ __device__ __forceinline__ float sumsq8(const uint32_t v[8], float acc) {
 
 // kPerLane > 0: rows of at most 64 * kPerLane blocks, whose first-pass loads
 // are all issued before any is used; kPerLane == 0: any row length.  The sum
-// is accumulated in the same order either way; the second pass re-reads the
-// row, which the first pass has just brought into the caches.
+// is accumulated in the same order either way.  With kPerLane > 0 the
+// second pass works on the registers of the first (X read once); otherwise
+// it re-reads the row.  (Waves that walk several rows with the next row's
+// loads in flight measured 12-22% slower at 8192 x 5120 than a wave per
+// row: the doubled registers cut the resident waves.)
 template <int kPerLane>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_quant_kernel(
     const uint16_t* __restrict__ x, uint32_t M, uint32_t K, uint32_t ldx, const uint16_t* __restrict__ gamma,
@@ -86,8 +89,8 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_quant_kernel(
   const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)row * ldx);
 
   float ss = 0.0f;
+  uint4 d[kPerLane > 0 ? kPerLane : 1][2];
   if constexpr (kPerLane > 0) {
-    uint4 d[kPerLane][2];
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) {
       const uint32_t b = lane + 64u * j;
@@ -118,10 +121,25 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_quant_kernel(
   uint2* codes_row = reinterpret_cast<uint2*>(codes + (size_t)row * (K >> 1));
   uint8_t* scales_row = scales + (size_t)row * nb;
   uint4* y_row = y == nullptr ? nullptr : reinterpret_cast<uint4*>(y + (size_t)row * ldy);
+  const float gd6 = g * (1.0f / 6.0f);
+  auto pass2 = [&](auto huge_tag) {
+    constexpr bool kHuge = decltype(huge_tag)::value;
+    if constexpr (kPerLane > 0) {
+      // From the registers of pass 1: X is read from memory once.
+#pragma unroll
+      for (int j = 0; j < kPerLane; ++j) {
+        const uint32_t b = lane + 64u * j;
+        if (b < nb) norm_quant_block<kHuge>(d[j][0], d[j][1], b, gr, r, g, gd6, codes_row, scales_row, y_row);
+      }
+    } else {
+      for (uint32_t b = lane; b < nb; b += 64)
+        norm_quant_block<kHuge>(xr[2 * b], xr[2 * b + 1], b, gr, r, g, gd6, codes_row, scales_row, y_row);
+    }
+  };
   if (g > kHugeScale)
-    norm_quant_row<true>(xr, gr, nb, r, g, codes_row, scales_row, y_row, lane);
+    pass2(std::integral_constant<bool, true>{});
   else
-    norm_quant_row<false>(xr, gr, nb, r, g, codes_row, scales_row, y_row, lane);
+    pass2(std::integral_constant<bool, false>{});
 }
 
 hipError_t launch_rmsnorm_quant(const void* x, int64_t M, int64_t K, int64_t ldx, const void* gamma,
