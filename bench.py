@@ -153,6 +153,22 @@ def measure_workload(name, steps, warmup, dev, log_fn):
         "act_quant_frac_hbm": round(aq_bytes / (aq_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "tflops_incl_act_quant": round(cfg.flops / ((aq_ms + gemm_ms) * 1e-3) / 1e12, 2),
     }
+    if cfg.n <= 96 and cfg.n % 2 == 0 and cfg.k % 64 == 0 and len(cfg.segments) == 2:
+        # The b|a gate projection with the GDN gate transform (Eq. 1) in the
+        # GEMM's epilogue, timed like the plain GEMM.
+        h = cfg.n // 2
+        rng = np.random.default_rng(99)
+        a_log = torch.from_numpy(np.log(rng.uniform(1.0, 16.0, h)).astype(np.float32)).to(dev)
+        dt_bias = torch.from_numpy(rng.uniform(-4.0, 2.0, h).astype(np.float32)).to(dev)
+        for _ in range(warmup):
+            L.gemm_gdn_gates(aq, pw, a_log, dt_bias, out=y)
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for i in range(steps):
+            gev[i][0].record(stream)
+            L.gemm_gdn_gates(aq, pw, a_log, dt_bias, out=y)
+            gev[i][1].record(stream)
+        torch.cuda.synchronize()
+        out["gemm_gdn_gates_avg_ms"] = round(float(np.mean([a.elapsed_time(b) for a, b in gev])), 4)
     if cfg.n <= 128 and cfg.k % 64 == 0:
         # Narrow output: act-quant fused into the GEMM, calibrated G (one pass
         # over X) and dynamic G (amax pass + one fused launch).
