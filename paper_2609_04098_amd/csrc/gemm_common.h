@@ -40,8 +40,9 @@
 //  * gemm_splitk_kernel (N <= 96, the tall-skinny gate projections; M <= 32,
 //    decode shapes): the output has too few 32 x 32 tiles to fill the chip,
 //    so the four waves of a workgroup share one tile and split its
-//    reduction, each streaming its chunks through a private LDS ring; the
-//    partial sums meet in LDS.
+//    reduction, each streaming its weight chunks through a private LDS ring
+//    and the activation, whole 128-byte row lines of 4 chunks, through a
+//    ring shared by the workgroup; the partial sums meet in LDS.
 //  * gemm_reg_kernel (K % 64 != 0, N > 96): operands go straight from global
 //    memory to registers one chunk ahead; per-block masking of the scales
 //    handles a K tail.
@@ -335,6 +336,28 @@ struct SplitkStage {
   static constexpr int kBytes = kScaleB + kPairsB * 256;
   static constexpr int kLoads = FM + FN + kPairsA + kPairsB;
 };
+
+// Shared activation stage of the split-K kernel (streamed activation, FM
+// fragments of 32 rows): one 128-byte line group per row (4 chunks of codes)
+// as FM * 4 slices of 8 rows (1 KB images), then per slice the 16 bytes of
+// scales of its 8 rows in a 260-byte slot (128 bytes of scales, 128 bytes of
+// zeros from the lanes without a row, 4 bytes that shift the next slot's
+// banks).  Each of the 4 waves loads FM slices.
+template <int FM>
+struct SplitkAGroup {
+  static constexpr int kSlices = 4 * FM, kSlicesPerWave = FM;
+  static constexpr int kScaleBase = kSlices * 1024, kScaleSlot = 260;
+  static constexpr int kBytes = (kScaleBase + kSlices * kScaleSlot + 15) / 16 * 16;
+  static constexpr int kLoadsPerWave = 2 * kSlicesPerWave;
+};
+
+// LDS of the split-K kernel: KS private weight rings, then the shared
+// activation ring (streamed activation) or nothing (the fused quantizer puts
+// its activation after the rings).
+template <int KS, int FM, int FN, int kStages, bool kAShared>
+constexpr int splitk_ring_bytes() {
+  return KS * kStages * SplitkStage<0, FN>::kBytes + (kAShared ? kStages * SplitkAGroup<FM>::kBytes : 0);
+}
 
 // Operands of one GEMM call (device pointers), as passed to the launchers.
 struct GemmOperands {

@@ -76,11 +76,13 @@ def test_gemm_tiny_workload():
     (70, 64, 192, [0, 64]),                # tall-skinny split-K: fewer chunks than waves
     (33, 90, 80, [0, 30, 90]),             # tall-skinny split-K, unaligned K, ragged N
     (513, 520, 1024, [0, 100, 200, 300, 400, 500, 510, 515, 520]),   # 8 segments
-    (32, 520, 5120, [0, 260, 520]),        # small-M split-K: 80 chunks over 8 waves, ragged N
+    (32, 520, 5120, [0, 260, 520]),        # small-M split-K: 80 chunks over 4 waves, ragged N
     (1, 300, 1040, [0, 300]),              # small-M, one row, K % 64 != 0
-    (17, 4100, 128, [0, 4000, 4100]),      # small-M, many column tiles, 2 chunks < 8 waves
+    (17, 4100, 128, [0, 4000, 4100]),      # small-M, many column tiles, 2 chunks < 4 waves
     (777, 1300, 384, [0, 500, 1300]),      # prefill path: 4 x 6 tiles of 256 x 256, ragged M and N
     (40, 96, 768, [0, 48, 96]),            # tall-skinny split-K: 3 chunks per wave (= ring stages)
+    (9, 200, 320, [0, 100, 200]),          # small-M, shared activation ring: 5 chunks, 3 waves idle in step 2
+    (8, 200, 320, [0, 100, 200]),          # small-M, private activation rings (the largest such M)
     (5, 200, 1024, [0, 100, 200]),         # small-M split-K: 4 chunks per wave (one refill)
     (9, 64, 960, [0, 64]),                 # split-K: 15 chunks, 4/4/4/3 per wave
 ])

@@ -144,6 +144,45 @@ def test_act_quant_exact_ties():
     assert_act_matches(xb, g=np.float32(0.5))
 
 
+def near_midpoint_blocks(g, rng_scales):
+    """Blocks [amax, x, -x, 0, ...] whose scale is S and whose x has |x| G / S
+    within 2^-19 (relative) of an E2M1 rounding midpoint without being on it."""
+    from oracle.formats import E4M3_GRID, bf16_bits_to_f64
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    s = E4M3_GRID[rng_scales]
+    target = mids[None, :] * s[:, None] / float(g)
+    base = bits_of(target).astype(np.int64)
+    blocks = []
+    for d in (-1, 0, 1):
+        xb = (base + d).astype(np.uint16)
+        q = bf16_bits_to_f64(xb) * float(g) / s[:, None]          # exact: 8 x 24 bits, S a power-of-two multiple
+        rel = np.abs(q - mids[None, :]) / mids[None, :]
+        for i, j in zip(*np.nonzero((rel > 0) & (rel < 2.0 ** -19))):
+            blk = np.zeros(16, dtype=np.uint16)
+            blk[0] = bits_of([6.0 * s[i] / float(g)])[0]           # rounds back to S
+            blk[1] = xb[i, j]
+            blk[2] = xb[i, j] | 0x8000
+            blocks.append(blk)
+    return blocks
+
+
+def test_act_quant_near_midpoints():
+    """Elements whose exact |x| G / S lies within 2^-19 of an E2M1 midpoint,
+    on either side of it: a quotient rounded anywhere before the decision
+    could land on the wrong side."""
+    rng = np.random.default_rng(2024)
+    found = 0
+    for trial in range(400):
+        g = np.float32(rng.uniform(1.0, 2.0) * 2.0 ** int(rng.integers(-4, 5)))
+        blocks = near_midpoint_blocks(g, np.arange(40, 120))
+        if not blocks:
+            continue
+        found += len(blocks)
+        xb = np.concatenate(blocks).reshape(-1, 16 * len(blocks))
+        assert_act_matches(xb, g=g)
+    assert found >= 20, found
+
+
 def test_act_quant_empty():
     g = torch.full((1,), 7.0, dtype=torch.float32, device="cuda")
     ws = L.act_workspace(0, 64, "cuda")
