@@ -100,6 +100,8 @@ def _case(seed, m, k, outliers=True):
     (33, 80, None, 1e-5, 0.6),         # K / 16 = 5 blocks < 64 lanes; G too small: saturation
     (8, 5120, 5184, 1e-6, 3.0),        # strided rows; G too large: many small codes
     (5, 17408, None, 0.0, 1.0),        # the MLP-down width, eps = 0
+    (3000, 1040, None, 1e-6, 1.0),     # more rows than the streaming grid's waves: waves walk rows
+    (20, 8192, 8200, 1e-6, 1.0),       # the longest row held in registers (16 KB LDS slot), strided
 ])
 def test_fused_matches_oracle(m, k, ldx, eps, gfac):
     x, gamma = _case(m + k, m, k)
