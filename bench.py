@@ -124,17 +124,18 @@ def measure_workload(name, steps, warmup, dev, log_fn):
     pw = L.pack_weight(to_dev(synth.make_w(cfg)), cfg.seg_offsets)
     aq = L.alloc_act(cfg.m, cfg.k, dev)
     ws = L.act_workspace(cfg.m, cfg.k, dev)
+    gws = L.gemm_workspace(cfg.m, cfg.n, cfg.k, dev)
     y = torch.empty((cfg.m, cfg.n), dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
         L.quantize_act(x, out=aq, workspace=ws)
-        L.gemm(aq, pw, out=y)
+        L.gemm(aq, pw, out=y, workspace=gws)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     for i in range(steps):
         ev[i][0].record(stream)
         L.quantize_act(x, out=aq, workspace=ws)
         ev[i][1].record(stream)
-        L.gemm(aq, pw, out=y)
+        L.gemm(aq, pw, out=y, workspace=gws)
         ev[i][2].record(stream)
     torch.cuda.synchronize()
     aq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
@@ -298,6 +299,7 @@ def main():
     aq = L.alloc_act(cfg.m, cfg.k, dev)
     ws = L.act_workspace(cfg.m, cfg.k, dev)
     y = torch.empty((cfg.m, cfg.n), dtype=torch.bfloat16, device=dev)
+    gws = L.gemm_workspace(cfg.m, cfg.n, cfg.k, dev)
 
     def step(ev=None):
         if ev is not None:
@@ -305,7 +307,7 @@ def main():
         L.quantize_act(x, out=aq, workspace=ws)
         if ev is not None:
             ev[1].record(stream)
-        L.gemm(aq, pw, out=y)
+        L.gemm(aq, pw, out=y, workspace=gws)
         if ev is not None:
             ev[2].record(stream)
 

@@ -241,15 +241,52 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                void* y, int64_t ldy, int y_dtype, void* stream);
 
 /*
- * Which kernels nvfp4_gemm launches for an M x N x K call on the current
- * device (diagnostics: benchmarks and profiles name the kernel they time).
- * part 0: the first launch; part 1: the second launch of a shape whose last
- * round of tiles runs as narrower tiles.  Returns a static string naming the
- * kernel and its tile shape, or NULL when that launch does not exist (M == 0,
- * no second launch) or the arguments are invalid (K % 16 != 0, N < 1,
- * M < 0, part not 0 or 1) or the device cannot be queried.
+ * Workspace bytes that let nvfp4_gemm_with_workspace run an M x N x K call
+ * in its K-halves form on the current device; 0 when the shape does not use
+ * it (then any workspace, or none, gives the nvfp4_gemm launches) or the
+ * arguments are invalid.  The form applies when the last round of 256 x 256
+ * output tiles (one per compute unit) would be at most half full, those
+ * tiles make whole tile columns, and K % 512 == 0 (e.g. 8192 x 5120 x 17408:
+ * 2 * 8192 * 1024 * 4 bytes).
  */
-const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part);
+size_t nvfp4_gemm_workspace(int64_t M, int64_t N, int64_t K);
+
+/*
+ * nvfp4_gemm with a caller workspace (same arguments, same result contract
+ * up to the summation order).  For shapes where nvfp4_gemm_workspace is
+ * non-zero, the output tiles of the partially filled last round are computed
+ * as two K halves on twice as many compute units: each half writes its
+ * segment-scaled FP32 partial sums to the workspace ([2][M][tail columns]),
+ * and a second pass writes y = half0 + half1 (one FP32 addition; bf16 output
+ * is that sum rounded to nearest even).  Three launches on `stream` instead
+ * of two; the workspace is overwritten and must not be used by another call
+ * in flight.
+ *   workspace        device memory, 16-byte aligned, or NULL when
+ *                    nvfp4_gemm_workspace(M, N, K) is 0.
+ *   workspace_bytes  its size.
+ * Errors: as nvfp4_gemm; NVFP4_EWORKSPACE if the workspace is smaller than
+ * nvfp4_gemm_workspace(M, N, K); NVFP4_EINVAL for a misaligned workspace.
+ */
+int nvfp4_gemm_with_workspace(const uint8_t* a_codes, const uint8_t* a_scales,
+                              const float* a_g_enc, int64_t M, int64_t K,
+                              const void* w_packed, int64_t N,
+                              const int64_t* seg_offsets, int n_seg, const float* w_g_enc_seg,
+                              void* y, int64_t ldy, int y_dtype,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Which kernels an M x N x K GEMM launches on the current device
+ * (diagnostics: benchmarks and profiles name the kernel they time), for
+ * nvfp4_gemm (with_workspace = 0) or nvfp4_gemm_with_workspace given a
+ * sufficient workspace (with_workspace = 1).  part 0: the first launch;
+ * part 1: the launch(es) of a shape whose partially filled last round of
+ * tiles runs in another form.  Returns a static string naming the kernel
+ * and its tile shape, or NULL when that launch does not exist (M == 0, no
+ * second launch) or the arguments are invalid (K % 16 != 0, N < 1, M < 0,
+ * part not 0 or 1, with_workspace not 0 or 1) or the device cannot be
+ * queried.
+ */
+const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part, int with_workspace);
 
 /*
  * The fused GDN gate projection with the gate transform in its epilogue

@@ -225,9 +225,10 @@ int nvfp4_harmonize_weight(void* packed, int64_t N, int64_t K, const int64_t* se
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 
-int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
-               int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
-               const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype, void* stream) {
+// Argument checks shared by nvfp4_gemm and nvfp4_gemm_with_workspace.
+static int check_gemm_args(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
+                           int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
+                           const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype) {
   if (y_dtype != NVFP4_BF16 && y_dtype != NVFP4_F32) return NVFP4_EINVAL;
   if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return NVFP4_EINVAL;
   if (ldy < N) return NVFP4_EINVAL;
@@ -244,18 +245,53 @@ int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g
     const uintptr_t elem = y_dtype == NVFP4_F32 ? 4u : 2u;
     if (reinterpret_cast<uintptr_t>(y) % elem) return NVFP4_EINVAL;
   }
-  int st = check_device();
+  return NVFP4_OK;
+}
+
+int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
+               int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
+               const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype, void* stream) {
+  int st = check_gemm_args(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg, w_g_enc_seg, y, ldy,
+                           y_dtype);
+  if (st != NVFP4_OK) return st;
+  st = check_device();
   if (st != NVFP4_OK) return st;
   hipError_t e = nvfp4::launch_gemm(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg,
-                                    w_g_enc_seg, y, ldy, y_dtype == NVFP4_F32,
+                                    w_g_enc_seg, y, ldy, y_dtype == NVFP4_F32, nullptr, 0,
                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? NVFP4_OK : fail_hip(e);
 }
 
-const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part) {
+size_t nvfp4_gemm_workspace(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0) return 0;
+  if (M * K >= kI32Lim || N * K >= kI32Lim) return 0;
+  if (check_device() != NVFP4_OK) return 0;
+  return nvfp4::gemm_workspace_bytes(M, N, K);
+}
+
+int nvfp4_gemm_with_workspace(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,
+                              int64_t K, const void* w_packed, int64_t N, const int64_t* seg_offsets, int n_seg,
+                              const float* w_g_enc_seg, void* y, int64_t ldy, int y_dtype, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  int st = check_gemm_args(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg, w_g_enc_seg, y, ldy,
+                           y_dtype);
+  if (st != NVFP4_OK) return st;
+  if (workspace != nullptr && !aligned16(workspace)) return NVFP4_EINVAL;
+  st = check_device();
+  if (st != NVFP4_OK) return st;
+  const size_t need = M > 0 ? nvfp4::gemm_workspace_bytes(M, N, K) : 0;
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return NVFP4_EWORKSPACE;
+  hipError_t e = nvfp4::launch_gemm(a_codes, a_scales, a_g_enc, M, K, w_packed, N, seg_offsets, n_seg,
+                                    w_g_enc_seg, y, ldy, y_dtype == NVFP4_F32, need > 0 ? workspace : nullptr,
+                                    workspace_bytes, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? NVFP4_OK : fail_hip(e);
+}
+
+const char* nvfp4_gemm_kernel(int64_t M, int64_t N, int64_t K, int part, int with_workspace) {
   if (M < 0 || N < 1 || K < NVFP4_BLOCK || K % NVFP4_BLOCK != 0 || (part != 0 && part != 1)) return nullptr;
+  if (with_workspace != 0 && with_workspace != 1) return nullptr;
   if (check_device() != NVFP4_OK) return nullptr;
-  return nvfp4::gemm_kernel_for(M, N, K, part);
+  return nvfp4::gemm_kernel_for(M, N, K, part, with_workspace == 1);
 }
 
 int nvfp4_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g_enc, int64_t M,

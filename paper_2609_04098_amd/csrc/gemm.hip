@@ -26,7 +26,7 @@ static uint32_t cu_count() {
 
 // The kernels one nvfp4_gemm call launches for a shape (n_cu: compute units
 // of the device).
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu, bool with_ws) {
   GemmPlan g{};
   g.n_split = (uint32_t)N;
   const bool aligned = (K % 64) == 0;
@@ -39,16 +39,19 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu) {
   } else if (aligned) {
     // Square tiles fill whole rounds of one workgroup per CU.  When the last
     // round would be at most half full and its tiles make whole tile
-    // columns, those columns run as a second launch of 256 x 128 tiles (two
-    // per CU), which takes about half a round instead of a full one.
-    // Scale super-stages need K % 256 == 0 (whole groups of 4 chunks).
+    // columns, those columns run as a second launch: with a workspace and
+    // K % 512 == 0, the same square tiles as two K halves on twice the CUs
+    // (FP32 partial sums, then a summing pass: about 0.55 of a round plus
+    // the pass); otherwise as 256 x 128 tiles (two per CU), about 0.7 of a
+    // round.  Scale super-stages need K % 256 == 0 (whole groups of 4
+    // chunks).
     g.first = (K % 256) == 0 ? GemmPlan::kLdsSuper : GemmPlan::kLdsSquare;
     const uint32_t tiles_m = (uint32_t)((M + kSquareTile - 1) / kSquareTile);
     const uint32_t tiles_n = (uint32_t)((N + kSquareTile - 1) / kSquareTile);
     const uint32_t rem = n_cu ? (tiles_m * tiles_n) % n_cu : 0;
     if (rem != 0 && rem <= n_cu / 2 && rem % tiles_m == 0 && rem / tiles_m < tiles_n) {
       g.n_split = (tiles_n - rem / tiles_m) * kSquareTile;
-      g.second = GemmPlan::kLdsTall;
+      g.second = (with_ws && K % 512 == 0) ? GemmPlan::kLdsSuperHalves : GemmPlan::kLdsTall;
     }
   } else {
     g.first = GemmPlan::kReg;
@@ -56,11 +59,18 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu) {
   return g;
 }
 
+size_t plan_workspace_bytes(const GemmPlan& g, int64_t M, int64_t N) {
+  if (g.second != GemmPlan::kLdsSuperHalves) return 0;
+  return (size_t)2 * (size_t)M * (size_t)halves_row((uint32_t)N - g.n_split) * sizeof(float);
+}
+
 const char* gemm_kernel_name(int kind) {
   switch (kind) {
     case GemmPlan::kLdsSquare: return "gemm_lds_kernel<LdsSquare> (256x256 tiles)";
     case GemmPlan::kLdsSuper: return "gemm_lds_kernel<LdsSquareSuper> (256x256 tiles, scale super-stages)";
     case GemmPlan::kLdsTall: return "gemm_lds_kernel<LdsTall> (256x128 tiles)";
+    case GemmPlan::kLdsSuperHalves:
+      return "gemm_lds_kernel<LdsSquareSuper> (256x256 tiles, two K halves, FP32 partials) + sum_halves_kernel";
     case GemmPlan::kSplitkNarrow: return "gemm_splitk_kernel<4,2,3,3> (64x96 tiles, split-K)";
     case GemmPlan::kSplitkDecode: return "gemm_splitk_kernel<4,1,2,3> (32x64 tiles, split-K)";
     case GemmPlan::kReg: return "gemm_reg_kernel<2,2,4,4> (256x256 tiles, register path)";
@@ -68,10 +78,10 @@ const char* gemm_kernel_name(int kind) {
   }
 }
 
-const char* gemm_kernel_for(int64_t M, int64_t N, int64_t K, int part) {
+const char* gemm_kernel_for(int64_t M, int64_t N, int64_t K, int part, bool with_ws) {
   const uint32_t n_cu = cu_count();
   if (n_cu == 0) return nullptr;
-  const GemmPlan g = plan_gemm(M, N, K, n_cu);
+  const GemmPlan g = plan_gemm(M, N, K, n_cu, with_ws);
   const int kind = part == 0 ? g.first : g.second;
   return kind == GemmPlan::kNone ? nullptr : gemm_kernel_name(kind);
 }
@@ -91,18 +101,32 @@ static hipError_t run_one(int kind, const GemmOperands& o, const GemmParams& p, 
   }
 }
 
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  const uint32_t n_cu = cu_count();
+  if (n_cu == 0 || M == 0) return 0;
+  return plan_workspace_bytes(plan_gemm(M, N, K, n_cu, true), M, N);
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                        int64_t M, int64_t K, const void* w_packed, int64_t N,
                        const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
-                       int64_t ldy, bool out_f32, hipStream_t stream) {
+                       int64_t ldy, bool out_f32, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 0) return hipSuccess;
   GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
   p.y_pairs = (ldy % 2 == 0) && (reinterpret_cast<uintptr_t>(y) % 4 == 0) ? 1u : 0u;
   const GemmOperands o{a_codes, a_scales, a_g, static_cast<const uint8_t*>(w_packed), w_g, y};
-  const GemmPlan g = plan_gemm(M, N, K, cu_count());
+  GemmPlan g = plan_gemm(M, N, K, cu_count(), workspace != nullptr);
+  if (g.second == GemmPlan::kLdsSuperHalves && workspace_bytes < plan_workspace_bytes(g, M, N))
+    g = plan_gemm(M, N, K, cu_count(), false);
   const bool aligned = (K % 64) == 0;
   hipError_t e = run_one(g.first, o, p, 0, g.n_split, out_f32, aligned, stream);
   if (e != hipSuccess || g.second == GemmPlan::kNone) return e;
+  if (g.second == GemmPlan::kLdsSuperHalves) {
+    float* parts = static_cast<float*>(workspace);
+    e = launch_lds_super_halves(o, p, g.n_split, (uint32_t)N, parts, stream);
+    if (e != hipSuccess) return e;
+    return launch_sum_halves(parts, (uint32_t)M, (uint32_t)N - g.n_split, y, (uint32_t)ldy, g.n_split, out_f32, stream);
+  }
   return run_one(g.second, o, p, g.n_split, (uint32_t)N, out_f32, aligned, stream);
 }
 

@@ -85,6 +85,10 @@ struct GemmParams {
   int n_seg;
   uint32_t seg_off[NVFP4_SEG_TABLE];
   uint32_t y_pairs;          // bf16 output: y and ldy allow dword stores of column pairs
+  // K split across workgroups (LDS kernel, FP32 output only): k_parts = 2
+  // runs every tile twice, workgroup 2t + j on chunks [j * chunks, (j + 1) *
+  // chunks) writing its partial sums at y + j * part_stride floats.
+  uint32_t k_parts, part_stride;
   // GDN gate epilogue (split-K kernel only): H b-columns, then H a-columns.
   const float* gate_a_log;
   const float* gate_dt_bias;
@@ -160,9 +164,9 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 // Tile (tm, tn) of workgroup blockIdx.x: XCD-contiguous remap (workgroup i
 // runs on XCD i % 8), then M-grouped order (kGroupM tiles of M per group).
 template <int kGroupM>
-__device__ __forceinline__ void tile_of(const GemmParams& p, uint32_t& tm, uint32_t& tn) {
+__device__ __forceinline__ void tile_of(const GemmParams& p, uint32_t& tm, uint32_t& tn,
+                                        uint32_t pid0 = blockIdx.x) {
   const uint32_t total = p.tiles_m * p.tiles_n;
-  const uint32_t pid0 = blockIdx.x;
   const uint32_t xcd = pid0 % kNumXcd, per = total / kNumXcd, extra = total % kNumXcd;
   const uint32_t pid = xcd * per + (xcd < extra ? xcd : extra) + pid0 / kNumXcd;
   const uint32_t in_group = kGroupM * p.tiles_n;
@@ -384,6 +388,8 @@ inline GemmParams gemm_params(int64_t M, int64_t K, int64_t N, const int64_t* se
   p.a_code_bytes = (uint32_t)(M * K / 2);
   p.a_scale_bytes = (uint32_t)(M * K / 16);
   p.w_bytes = (uint32_t)d.bytes;
+  p.k_parts = 1;
+  p.part_stride = 0;
   p.n_seg = n_seg;
   for (int i = 0; i < NVFP4_SEG_TABLE; ++i)
     p.seg_off[i] = (uint32_t)seg_offsets[i <= n_seg ? i : n_seg];
@@ -396,11 +402,14 @@ constexpr uint32_t kSquareTile = 256;
 // The kernels one nvfp4_gemm call launches: `first` over output columns
 // [0, n_split), then `second` (if any) over [n_split, N).
 struct GemmPlan {
-  enum Kind { kNone = 0, kLdsSquare, kLdsSuper, kLdsTall, kSplitkNarrow, kSplitkDecode, kReg };
+  enum Kind { kNone = 0, kLdsSquare, kLdsSuper, kLdsTall, kSplitkNarrow, kSplitkDecode, kReg, kLdsSuperHalves };
   int first, second;
   uint32_t n_split;
 };
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu);
+// with_ws: the caller provides gemm_workspace_bytes of workspace (the last
+// round's tile columns may then run as two K halves on twice the CUs).
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu, bool with_ws);
+size_t plan_workspace_bytes(const GemmPlan& g, int64_t M, int64_t N);
 const char* gemm_kernel_name(int kind);
 
 // Launchers of the kernel families (each in its own translation unit).
@@ -411,6 +420,14 @@ hipError_t launch_lds_super_bf16(const GemmOperands& o, GemmParams p, uint32_t n
                                  hipStream_t stream);
 hipError_t launch_lds_super_f32(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end,
                                 hipStream_t stream);
+// The same kernel over columns [n_begin, n_end) with the K range split in
+// two halves (p.chunks % 8 == 0): FP32 partial sums (segment-scaled) to
+// parts[2][M][halves_row(n_end - n_begin)]; sum_halves then forms Y.
+inline uint32_t halves_row(uint32_t width) { return (width + 3u) & ~3u; }
+hipError_t launch_lds_super_halves(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end,
+                                   float* parts, hipStream_t stream);
+hipError_t launch_sum_halves(const float* parts, uint32_t M, uint32_t width, void* y, uint32_t ldy, uint32_t col0,
+                             bool out_f32, hipStream_t stream);
 hipError_t launch_lds_tall(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end, bool out_f32,
                            hipStream_t stream);
 // Split-K: 64 x 96 tiles (N <= 96, optional GDN gate epilogue), 32 x 64 tiles (M <= 32).

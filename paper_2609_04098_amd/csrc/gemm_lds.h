@@ -93,8 +93,13 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const uint32_t lane = threadIdx.x & 63, wave = wave_index();
   const uint32_t r = lane & 31, h = lane >> 5;
+  // K split (FP32 partial sums): workgroup 2t + part takes chunks
+  // [part * chunks, (part + 1) * chunks) of tile t; the descriptors' bases
+  // move to the first of them, the row strides stay those of the whole K.
+  const uint32_t part = p.k_parts > 1 ? (blockIdx.x & 1u) : 0u;
+  const uint32_t kc0 = part * p.chunks;
   uint32_t tm, tn;
-  tile_of<C::kGroupM>(p, tm, tn);
+  tile_of<C::kGroupM>(p, tm, tn, p.k_parts > 1 ? blockIdx.x >> 1 : blockIdx.x);
   const uint32_t wm = wave / WN, wn = wave % WN;
 
   // Per-lane offsets are fixed; the chunk advances the descriptors' base
@@ -128,10 +133,10 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   const uint8_t* w_scales = w_packed + p.w_scale_offset;
   const uint32_t w_scale_bytes = p.w_bytes - p.w_scale_offset;
 
-  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes, p.a_code_bytes);
-  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales, p.a_scale_bytes);
-  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed, p.w_scale_offset);
-  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales, w_scale_bytes);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(a_codes + kc0 * 32u, p.a_code_bytes - kc0 * 32u);
+  const __amdgpu_buffer_rsrc_t rs = rsrc(a_scales + kc0 * 4u, p.a_scale_bytes - kc0 * 4u);
+  const __amdgpu_buffer_rsrc_t rb = rsrc(w_packed + kc0 * 1024u, p.w_scale_offset - kc0 * 1024u);
+  const __amdgpu_buffer_rsrc_t rbs = rsrc(w_scales + kc0 * 128u, w_scale_bytes - kc0 * 128u);
   // DMA of chunk kc into stage kc % kStages.  The ring runs kStages - 1
   // chunks past the end of K; those stages are never read, and re-load the
   // last chunk so that every address stays inside its tensor.
@@ -312,7 +317,8 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   }
   // Drain the DMA of the chunks past the end before the workgroup exits.
   __builtin_amdgcn_s_waitcnt(0x0F70);
-  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, y, tm * BM + wm * FM * 32, p.n_off + tn * BN + wn * FN * 32, r, h);
+  void* yo = kF32Out ? static_cast<void*>(static_cast<float*>(y) + (size_t)part * p.part_stride) : y;
+  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, yo, tm * BM + wm * FM * 32, p.n_off + tn * BN + wn * FN * 32, r, h);
 }
 
 // Output columns [n_begin, n_end) (n_begin a multiple of 32).
@@ -322,7 +328,7 @@ static hipError_t launch_lds_as(const GemmOperands& o, GemmParams p, uint32_t n_
   p.n_off = n_begin;
   p.tiles_m = (p.M + C::BM - 1) / C::BM;
   p.tiles_n = (n_end - n_begin + C::BN - 1) / C::BN;
-  const dim3 grid(p.tiles_m * p.tiles_n), block(C::kThreads);
+  const dim3 grid(p.tiles_m * p.tiles_n * p.k_parts), block(C::kThreads);
   hipLaunchKernelGGL((gemm_lds_kernel<C, kF32Out>), grid, block, C::kLdsBytes, stream, o.a_codes, o.a_scales, o.a_g,
                      o.w_packed, o.w_g, o.y, p);
   return hipGetLastError();

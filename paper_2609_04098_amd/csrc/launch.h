@@ -51,14 +51,19 @@ hipError_t launch_harmonize_weight(void* packed, int64_t N, int64_t K, const int
                                    int n_seg, const float* g_enc_seg, float* g_shared,
                                    hipStream_t stream);
 
+// nvfp4_gemm and nvfp4_gemm_with_workspace: workspace may be null (then
+// workspace_bytes is ignored); a workspace of gemm_workspace_bytes(M, N, K)
+// bytes or more enables the K-halves form of a partial last round.
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                        int64_t M, int64_t K, const void* w_packed, int64_t N,
                        const int64_t* seg_offsets, int n_seg, const float* w_g, void* y,
-                       int64_t ldy, bool out_f32, hipStream_t stream);
+                       int64_t ldy, bool out_f32, void* workspace, size_t workspace_bytes, hipStream_t stream);
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 // Name of launch `part` (0 or 1) of launch_gemm for this shape on the
-// current device; NULL if that launch does not exist.
-const char* gemm_kernel_for(int64_t M, int64_t N, int64_t K, int part);
+// current device, with or without a sufficient workspace; NULL if that
+// launch does not exist.
+const char* gemm_kernel_for(int64_t M, int64_t N, int64_t K, int part, bool with_ws);
 
 hipError_t launch_gemm_gdn_gates(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_g,
                                  int64_t M, int64_t K, const void* w_packed, int64_t H, const float* w_g,

@@ -109,7 +109,28 @@ def rmsnorm_quantize_act(x, gamma, eps, g, out: QuantizedAct = None, y=None, str
     return aq
 
 
-def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None, stream=None):
+def gemm_workspace(m, n, k, device):
+    """Workspace for gemm() at this shape (None when the shape needs none)."""
+    nbytes = _c.nvfp4_gemm_workspace(m, n, k)
+    return None if nbytes == 0 else torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None, workspace=None, stream=None):
+    """Y = dq(A) dq(W)^T through nvfp4_gemm_with_workspace (a workspace is
+    allocated here when the shape uses one and none is given)."""
+    if aq.k != pw.k:
+        raise ValueError("K mismatch between activation and weight")
+    dev = aq.codes.device
+    y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=dev)
+    kind = _c.NVFP4_F32 if y.dtype == torch.float32 else _c.NVFP4_BF16
+    ws = gemm_workspace(aq.m, pw.n, aq.k, dev) if workspace is None else workspace
+    _c.nvfp4_gemm_with_workspace(aq.codes, aq.scales, aq.g, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, kind,
+                                 ws, stream, M=aq.m, K=aq.k)
+    return y
+
+
+def gemm_no_workspace(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None, stream=None):
+    """The same product through nvfp4_gemm (no workspace)."""
     if aq.k != pw.k:
         raise ValueError("K mismatch between activation and weight")
     y = out if out is not None else torch.empty((aq.m, pw.n), dtype=out_dtype, device=aq.codes.device)
@@ -119,9 +140,11 @@ def gemm(aq: QuantizedAct, pw: PackedWeight, out_dtype=torch.bfloat16, out=None,
     return y
 
 
-def gemm_kernels(m, n, k):
-    """Names of the kernels gemm() launches for an m x n x k call."""
-    return [name for name in (_c.nvfp4_gemm_kernel(m, n, k, part) for part in (0, 1)) if name is not None]
+def gemm_kernels(m, n, k, with_workspace=True):
+    """Names of the kernels gemm() (or, with_workspace=False,
+    gemm_no_workspace()) launches for an m x n x k call."""
+    w = 1 if with_workspace else 0
+    return [name for name in (_c.nvfp4_gemm_kernel(m, n, k, part, w) for part in (0, 1)) if name is not None]
 
 
 def gemm_gdn_gates(aq: QuantizedAct, pw: PackedWeight, a_log, dt_bias, out_dtype=torch.bfloat16, out=None,

@@ -41,7 +41,10 @@ SIGNATURES = {
                                  _vp, _sz, _vp]),
     "nvfp4_unpack_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _vp, _vp]),
     "nvfp4_harmonize_weight": (_int, [_vp, _c_int64, _c_int64, _vp, _int, _vp, _vp, _vp]),
-    "nvfp4_gemm_kernel": (ctypes.c_char_p, [_c_int64, _c_int64, _c_int64, _int]),
+    "nvfp4_gemm_workspace": (_sz, [_c_int64, _c_int64, _c_int64]),
+    "nvfp4_gemm_with_workspace": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
+                                         _c_int64, _int, _vp, _sz, _vp]),
+    "nvfp4_gemm_kernel": (ctypes.c_char_p, [_c_int64, _c_int64, _c_int64, _int, _int]),
     "nvfp4_gemm_gdn_gates": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _vp, _vp, _vp,
                                     _c_int64, _int, _vp]),
     "nvfp4_gemm": (_int, [_vp, _vp, _vp, _c_int64, _c_int64, _vp, _c_int64, _vp, _int, _vp, _vp,
@@ -185,10 +188,28 @@ def nvfp4_gemm(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg
     _check(st, "nvfp4_gemm")
 
 
-def nvfp4_gemm_kernel(M, N, K, part=0):
-    """Name of launch `part` of nvfp4_gemm for this shape on the current
-    device, or None."""
-    r = lib().nvfp4_gemm_kernel(int(M), int(N), int(K), int(part))
+def nvfp4_gemm_workspace(M, N, K):
+    return lib().nvfp4_gemm_workspace(int(M), int(N), int(K))
+
+
+def nvfp4_gemm_with_workspace(a_codes, a_scales, a_g_enc, w_packed, N, seg_offsets, w_g_enc_seg, y,
+                              y_dtype=NVFP4_BF16, workspace=None, stream=None, M=None, K=None):
+    """nvfp4_gemm with a workspace (uint8 device tensor or None)."""
+    M = a_codes.shape[0] if M is None else M
+    K = 2 * a_codes.shape[1] if K is None else K
+    offs, n_seg = _offsets(seg_offsets)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().nvfp4_gemm_with_workspace(_ptr(a_codes), _ptr(a_scales), _ptr(a_g_enc), M, K, _ptr(w_packed), N,
+                                         offs, n_seg, _ptr(w_g_enc_seg), _ptr(y), y.stride(0), y_dtype,
+                                         _ptr(workspace), ws_bytes, _stream(stream))
+    _check(st, "nvfp4_gemm_with_workspace")
+
+
+def nvfp4_gemm_kernel(M, N, K, part=0, with_workspace=0):
+    """Name of launch `part` of nvfp4_gemm (with_workspace 0) or of
+    nvfp4_gemm_with_workspace (1) for this shape on the current device, or
+    None."""
+    r = lib().nvfp4_gemm_kernel(int(M), int(N), int(K), int(part), int(with_workspace))
     return None if r is None else r.decode()
 
 

@@ -31,10 +31,11 @@ hipError_t launch_harmonize_weight(void*, int64_t, int64_t, const int64_t*, int,
   return hipErrorNoDevice;
 }
 hipError_t launch_gemm(const uint8_t*, const uint8_t*, const float*, int64_t, int64_t, const void*, int64_t,
-                       const int64_t*, int, const float*, void*, int64_t, bool, hipStream_t) {
+                       const int64_t*, int, const float*, void*, int64_t, bool, void*, size_t, hipStream_t) {
   return hipErrorNoDevice;
 }
-const char* gemm_kernel_for(int64_t, int64_t, int64_t, int) { return nullptr; }
+size_t gemm_workspace_bytes(int64_t, int64_t, int64_t) { return 0; }
+const char* gemm_kernel_for(int64_t, int64_t, int64_t, int, bool) { return nullptr; }
 hipError_t launch_gemm_gdn_gates(const uint8_t*, const uint8_t*, const float*, int64_t, int64_t, const void*, int64_t,
                                  const float*, const float*, const float*, void*, int64_t, bool, hipStream_t) {
   return hipErrorNoDevice;

@@ -117,6 +117,20 @@ def test_gemm_rejects_bad_arguments():
     assert f(FAKE, FAKE, FAKE, 16, 64, FAKE, 32, None, 1, FAKE, FAKE, 32, 0, None) == C.NVFP4_EINVAL
 
 
+def test_gemm_with_workspace_rejects_bad_arguments():
+    f = C.lib().nvfp4_gemm_with_workspace
+
+    def call(M=16, K=64, N=32, offs=(0, 32), n_seg=1, ldy=32, dtype=0, y=FAKE, ws=None, wsb=0):
+        return f(FAKE, FAKE, FAKE, M, K, FAKE, N, _offs(list(offs)), n_seg, FAKE, y, ldy, dtype, ws, wsb, None)
+    assert call(K=40) == C.NVFP4_EINVAL                     # the nvfp4_gemm checks come first
+    assert call(ldy=24) == C.NVFP4_EINVAL
+    assert call(y=None) == C.NVFP4_EINVAL
+    assert call(ws=FAKE + 8, wsb=1 << 20) == C.NVFP4_EINVAL  # misaligned workspace
+    # sizes: no device here (or a shape with full rounds): 0
+    assert C.lib().nvfp4_gemm_workspace(16, 32, 40) == 0     # invalid K
+    assert C.lib().nvfp4_gemm_workspace(-1, 32, 64) == 0
+
+
 def test_unpack_rejects_bad_arguments():
     f = C.lib().nvfp4_unpack_weight
     assert f(FAKE, 0, 32, FAKE, FAKE, None) == C.NVFP4_EINVAL
@@ -237,6 +251,8 @@ def test_valid_arguments_stop_at_the_device_check():
         lambda: lib.nvfp4_unpack_weight(FAKE, 96, 256, FAKE, FAKE, None),
         lambda: lib.nvfp4_harmonize_weight(FAKE, 96, 256, offs, 2, FAKE, FAKE + 64, None),
         lambda: lib.nvfp4_gemm(FAKE, FAKE, FAKE, 64, 256, FAKE, 96, offs, 2, FAKE, FAKE, 96, C.NVFP4_BF16, None),
+        lambda: lib.nvfp4_gemm_with_workspace(FAKE, FAKE, FAKE, 64, 256, FAKE, 96, offs, 2, FAKE, FAKE, 96,
+                                              C.NVFP4_BF16, None, 0, None),
         lambda: lib.nvfp4_gemm_gdn_gates(FAKE, FAKE, FAKE, 64, 256, FAKE, 48, FAKE, FAKE, FAKE, FAKE, 96,
                                          C.NVFP4_F32, None),
         lambda: lib.nvfp4_quantize_gemm(FAKE, 64, 256, 256, FAKE, C.NVFP4_STATIC, None, 0, FAKE, 96, offs, 2, FAKE,
@@ -244,8 +260,10 @@ def test_valid_arguments_stop_at_the_device_check():
     ]
     for call in calls:
         assert call() in (C.NVFP4_EHIP, C.NVFP4_EUNSUPPORTED)
-    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 0) is None
-    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 2) is None
+    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 0, 0) is None
+    assert lib.nvfp4_gemm_kernel(8192, 34816, 5120, 2, 0) is None
+    assert lib.nvfp4_gemm_kernel(8192, 5120, 17408, 1, 1) is None
+    assert lib.nvfp4_gemm_workspace(8192, 5120, 17408) == 0
 
 
 def test_quantize_act_noalloc_rejects_bad_arguments():

@@ -1,4 +1,5 @@
-"""GPU parity of the NVFP4 GEMM (nvfp4_gemm) against the CPU oracle.
+"""GPU parity of the NVFP4 GEMM (nvfp4_gemm_with_workspace, and nvfp4_gemm
+where the two differ) against the CPU oracle.
 
 FP32 output: per element |Y - Y_ref| <= 1e-4 * sum_k |a_k w_k| and relative
 Frobenius error <= 1e-5 (tests/gpu_common.py).  BF16 output: equal to the
@@ -13,6 +14,7 @@ import torch
 from oracle import gemm as OG
 from oracle import quant as OQ
 from paper_2609_04098_amd import linear as L
+from paper_2609_04098_amd import nvfp4 as C
 from paper_2609_04098_amd import synth
 from tests.gpu_common import bf16_rne_of, check_gemm, log, np_u8, to_dev_bf16, workload
 
@@ -23,16 +25,18 @@ def bits_of(v):
     return synth.f64_to_bf16_bits(np.asarray(v, dtype=np.float64))
 
 
-def run_gpu(x_bits, w_bits, offs, ldy=None):
-    """Quantize, pack and multiply on the GPU; returns (y32, y16 bits, aq, pw)."""
+def run_gpu(x_bits, w_bits, offs, ldy=None, use_ws=True):
+    """Quantize, pack and multiply on the GPU; returns (y32, y16 bits, aq, pw).
+    use_ws=False: through nvfp4_gemm (no workspace)."""
     m, n = x_bits.shape[0], w_bits.shape[0]
     aq = L.quantize_act(to_dev_bf16(x_bits))
     pw = L.pack_weight(to_dev_bf16(w_bits), offs)
     ldy = n if ldy is None else ldy
     y32 = torch.empty((m, ldy), dtype=torch.float32, device="cuda")[:, :n]
     y16 = torch.empty((m, ldy), dtype=torch.bfloat16, device="cuda")[:, :n]
-    L.gemm(aq, pw, out=y32)
-    L.gemm(aq, pw, out=y16)
+    mul = L.gemm if use_ws else L.gemm_no_workspace
+    mul(aq, pw, out=y32)
+    mul(aq, pw, out=y16)
     torch.cuda.synchronize()
     return y32, y16, aq, pw
 
@@ -93,24 +97,62 @@ def test_gemm_ragged_shapes(m, n, k, offs):
 
 
 @pytest.mark.parametrize("k", [128, 512])
-def test_gemm_tail_columns_as_narrow_tiles(k):
+@pytest.mark.parametrize("use_ws", [False, True])
+def test_gemm_tail_columns(k, use_ws):
     # 2 x 130 tiles of 256 x 256: on a 256-CU device the 4 tiles past two
-    # full rounds (two tile columns) run as 256 x 128 tiles in a second
-    # launch; ragged M and N inside that tail.  K = 512 runs the scale
-    # super-stage kernel for the first launch.  Every element is checked.
+    # full rounds (two tile columns) run as a second launch: 256 x 128 tiles
+    # (nvfp4_gemm, or K % 512 != 0), or, with a workspace and K = 512, the
+    # square tiles as two K halves (FP32 partials, then the summing pass).
+    # Ragged M and N (a tail 356 columns wide, not a multiple of 8) inside
+    # that tail.  K = 512 runs the scale super-stage kernel for the first
+    # launch.  Every element is checked.
     rng = np.random.default_rng(304 + k)
     m, n = 300, 129 * 256 + 100
     x, w = _xw(rng, m, n, k)
     offs = [0, 20000, 33000, n]
-    y32, y16, _, _ = run_gpu(x, w, offs)
+    y32, y16, _, _ = run_gpu(x, w, offs, use_ws=use_ws)
     xp, xs, gx = OQ.quantize_tensor(x)
     wp, ws, gw = OQ.quantize_segments(w, offs)
     y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs)
     r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
-    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "tail split K=%d" % k)
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "tail K=%d ws=%s" % (k, use_ws))
     np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
                                   bf16_rne_of(y32.contiguous()))
-    log("tail split K=%d: launches %s" % (k, L.gemm_kernels(m, n, k)))
+    kernels = L.gemm_kernels(m, n, k, with_workspace=use_ws)
+    log("tail K=%d ws=%s: launches %s" % (k, use_ws, kernels))
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert len(kernels) == 2
+        assert ("two K halves" in kernels[1]) == (use_ws and k % 512 == 0)
+
+
+def test_gemm_last_round_as_k_halves_one_tile():
+    """One tile row, (CUs + 1) tile columns: the single tile of the last
+    round runs as two K halves on two CUs (with a workspace), ragged segment
+    boundaries inside it; every element against the oracle, and the bf16
+    output equal to RNE of the FP32 output.  The workspace path and
+    nvfp4_gemm agree on every column outside that tile bit for bit."""
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    rng = np.random.default_rng(306)
+    m, n, k = 256, (ncu + 1) * 256, 1024
+    x, w = _xw(rng, m, n, k)
+    offs = [0, 1000, n - 100, n]
+    need = C.nvfp4_gemm_workspace(m, n, k)
+    assert need == 2 * m * 256 * 4
+    y32, y16, aq, pw = run_gpu(x, w, offs)
+    y_nows = L.gemm_no_workspace(aq, pw, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    xp, xs, gx = OQ.quantize_tensor(x)
+    wp, ws, gw = OQ.quantize_segments(w, offs)
+    y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs)
+    r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs)
+    check_gemm(y32.cpu().numpy().astype(np.float64), y_ref, r_ref, "K halves, one tile")
+    check_gemm(y_nows.cpu().numpy().astype(np.float64), y_ref, r_ref, "no workspace")
+    np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_of(y32.contiguous()))
+    assert torch.equal(y32[:, : n - 256], y_nows[:, : n - 256])
+    # a workspace one byte short is refused
+    with pytest.raises(C.Nvfp4Error):
+        L.gemm(aq, pw, out=y32, workspace=torch.empty(need - 1, dtype=torch.uint8, device="cuda"))
 
 
 def test_gemm_super_stage_every_element():
