@@ -8,15 +8,14 @@ namespace nvfp4 {
 // ------------------------------------------- fused quantize + tall-skinny GEMM
 //
 // For narrow outputs (N <= 128: the gate projections), the activation is
-// quantized inside the GEMM: each lane loads the 32 bf16 values it supplies
+// quantized inside the GEMM: each lane takes the 32 bf16 values it supplies
 // to the MFMA (row r, reduction indices [32h, 32h + 32) of the chunk: two
 // whole blocks), quantizes them with the same device code as the stand-alone
 // quantizer (so the codes are identical), optionally stores the codes and
 // scales, and feeds the decoded values to the MFMA; X is read once and the
-// codes never travel through memory.  Tile: 32 rows x FN fragments, the KS
-// waves of a workgroup split the reduction (wave w takes chunks w, w + KS,
-// ...), operands go straight to registers one chunk ahead, and the partial
-// sums meet in LDS (splitk_epilogue).  G_A is read (static) or formed from
+// codes never travel through memory.  Tile: FM x 32 rows x FN fragments, the
+// KS waves of a workgroup split the reduction (wave w takes chunks w,
+// w + KS, ...), and the partial sums meet in LDS (splitk_epilogue).  G_A is read (static) or formed from
 // the amax pass's partial maxima (dynamic; workgroup 0 writes it out), and
 // the epilogue uses the value, not the memory.  K % 64 == 0.
 //
