@@ -97,11 +97,11 @@ def _case(seed, m, k, outliers=True):
 
 @pytest.mark.parametrize("m,k,ldx,eps,gfac", [
     (64, 256, None, 1e-6, 1.0),        # G from the normalized tensor's amax
-    (33, 80, None, 1e-5, 0.6),         # K / 16 = 5 blocks < 64 lanes; G too small: saturation
+    (33, 80, None, 1e-5, 0.6),         # 5 blocks: the pair's second wave has none; odd M; G too small
     (8, 5120, 5184, 1e-6, 3.0),        # strided rows; G too large: many small codes
     (5, 17408, None, 0.0, 1.0),        # the MLP-down width, eps = 0
-    (3000, 1040, None, 1e-6, 1.0),     # more rows than the streaming grid's waves: waves walk rows
-    (20, 8192, 8200, 1e-6, 1.0),       # the longest row held in registers (16 KB LDS slot), strided
+    (3000, 1040, None, 1e-6, 1.0),     # 65 blocks: one block in the pair's second wave
+    (20, 8192, 8200, 1e-6, 1.0),       # the longest row held in registers (4 blocks per lane), strided
 ])
 def test_fused_matches_oracle(m, k, ldx, eps, gfac):
     x, gamma = _case(m + k, m, k)
