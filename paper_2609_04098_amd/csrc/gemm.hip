@@ -35,7 +35,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, uint32_t n_cu, bool with_ws)
   } else if (aligned && N <= 96) {
     g.first = GemmPlan::kSplitkNarrow;
   } else if (aligned && M <= 32) {
-    g.first = GemmPlan::kSplitkDecode;
+    g.first = M <= 8 ? GemmPlan::kSplitkDecodeFew : GemmPlan::kSplitkDecode;
   } else if (aligned) {
     // Square tiles fill whole rounds of one workgroup per CU.  When the last
     // round would be at most half full and its tiles make whole tile
@@ -72,7 +72,8 @@ const char* gemm_kernel_name(int kind) {
     case GemmPlan::kLdsSuperHalves:
       return "gemm_lds_kernel<LdsSquareSuper> (256x256 tiles, two K halves, FP32 partials) + sum_halves_kernel";
     case GemmPlan::kSplitkNarrow: return "gemm_splitk_kernel<4,2,3,3> (64x96 tiles, split-K)";
-    case GemmPlan::kSplitkDecode: return "gemm_splitk_kernel<4,1,2,3> (32x64 tiles, split-K)";
+    case GemmPlan::kSplitkDecode: return "gemm_splitk_kernel<4,1,2,3> (32x64 tiles, split-K, shared activation ring)";
+    case GemmPlan::kSplitkDecodeFew: return "gemm_splitk_kernel<4,1,1,3> (32x32 tiles, split-K, per-wave rings)";
     case GemmPlan::kReg: return "gemm_reg_kernel<2,2,4,4> (256x256 tiles, register path)";
     default: return "none";
   }
@@ -95,7 +96,8 @@ static hipError_t run_one(int kind, const GemmOperands& o, const GemmParams& p, 
                      : launch_lds_super_bf16(o, p, n_begin, n_end, stream);
     case GemmPlan::kLdsTall: return launch_lds_tall(o, p, n_begin, n_end, out_f32, stream);
     case GemmPlan::kSplitkNarrow: return launch_splitk_narrow(o, p, out_f32, false, stream);
-    case GemmPlan::kSplitkDecode: return launch_splitk_decode(o, p, out_f32, stream);
+    case GemmPlan::kSplitkDecode:
+    case GemmPlan::kSplitkDecodeFew: return launch_splitk_decode(o, p, out_f32, stream);
     case GemmPlan::kReg: return launch_reg_square(o, p, out_f32, aligned, stream);
     default: return hipSuccess;
   }

@@ -402,7 +402,8 @@ constexpr uint32_t kSquareTile = 256;
 // The kernels one nvfp4_gemm call launches: `first` over output columns
 // [0, n_split), then `second` (if any) over [n_split, N).
 struct GemmPlan {
-  enum Kind { kNone = 0, kLdsSquare, kLdsSuper, kLdsTall, kSplitkNarrow, kSplitkDecode, kReg, kLdsSuperHalves };
+  enum Kind { kNone = 0, kLdsSquare, kLdsSuper, kLdsTall, kSplitkNarrow, kSplitkDecode, kReg, kLdsSuperHalves,
+              kSplitkDecodeFew };
   int first, second;
   uint32_t n_split;
 };
@@ -430,9 +431,13 @@ hipError_t launch_sum_halves(const float* parts, uint32_t M, uint32_t width, voi
                              bool out_f32, hipStream_t stream);
 hipError_t launch_lds_tall(const GemmOperands& o, GemmParams p, uint32_t n_begin, uint32_t n_end, bool out_f32,
                            hipStream_t stream);
-// Split-K: 64 x 96 tiles (N <= 96, optional GDN gate epilogue), 32 x 64 tiles (M <= 32).
+// Split-K: 64 x 96 tiles (N <= 96, optional GDN gate epilogue); M <= 32:
+// 32 x 32 tiles (M <= 8) or 32 x 64 tiles.
 hipError_t launch_splitk_narrow(const GemmOperands& o, GemmParams p, bool out_f32, bool gate, hipStream_t stream);
 hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f32, hipStream_t stream);
+// Largest activation (in 16-element blocks) the fused decode launch
+// quantizes inside every workgroup: 1024 blocks = M * K <= 16384 elements.
+constexpr uint32_t kDecodeFuseMaxBlocks = 1024;
 // Activation quantization fused in front of the M <= 32 split-K GEMM, one
 // launch, with the whole quantized activation held in LDS (see
 // gemm_splitk.hip); decode_quant_lds_bytes(M, K) is the LDS it takes.

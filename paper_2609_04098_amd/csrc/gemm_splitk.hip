@@ -65,20 +65,30 @@ __device__ __forceinline__ void load_x_block(const DecodeQuantArgs& q, uint32_t 
 }
 
 // Quantize all of X into the LDS activation (codes [M][K/2], then scales
-// [M][K/16]); returns G.
+// [M][K/16]); returns G.  X has at most kDecodeFuseMaxBlocks blocks (the
+// launcher's bound): each thread loads its blocks once and keeps them in
+// registers from the maximum to the quantization.
 template <int kThreads, bool kDynamic>
 __device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p, uint8_t* lds_codes,
                                    uint8_t* lds_scales, uint32_t* red) {
+  constexpr int kSlots = kDecodeFuseMaxBlocks / kThreads;
+  static_assert(kSlots * kThreads == kDecodeFuseMaxBlocks, "blocks per thread");
   const uint32_t bpr = p.K >> 4, n_blocks = p.M * bpr;
+  uint32_t v[kSlots][8];
+  uint32_t m = 0;
+#pragma unroll
+  for (int t = 0; t < kSlots; ++t) {
+    const uint32_t b = threadIdx.x + t * kThreads;
+    if (b < n_blocks) {
+      load_x_block(q, b, bpr, v[t]);
+      if (kDynamic) {
+        const uint32_t a = __float_as_uint(block_amax(v[t]));
+        m = m > a ? m : a;                   // non-negative floats order as integers
+      }
+    }
+  }
   float g;
   if (kDynamic) {
-    uint32_t m = 0;
-    for (uint32_t b = threadIdx.x; b < n_blocks; b += kThreads) {
-      uint32_t v[8];
-      load_x_block(q, b, bpr, v);
-      const uint32_t a = __float_as_uint(block_amax(v));
-      m = m > a ? m : a;                     // non-negative floats order as integers
-    }
     g = global_scale(__uint_as_float(wg_max_u32<kThreads>(m, red)));
     if (blockIdx.x == 0 && threadIdx.x == 0) *q.g_enc = g;
   } else {
@@ -86,18 +96,21 @@ __device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p
   }
   const float gd6 = g * (1.0f / 6.0f);
   const bool out = q.codes != nullptr && blockIdx.x == 0;
-  for (uint32_t b = threadIdx.x; b < n_blocks; b += kThreads) {
-    uint32_t v[8], c0, c1, sc;
-    load_x_block(q, b, bpr, v);
-    if (g > kHugeScale)
-      sc = quantize_block<true>(v, g, gd6, c0, c1);
-    else
-      sc = quantize_block<false>(v, g, gd6, c0, c1);
-    reinterpret_cast<uint2*>(lds_codes)[b] = make_uint2(c0, c1);
-    lds_scales[b] = (uint8_t)sc;
-    if (out) {
-      reinterpret_cast<uint2*>(q.codes)[b] = make_uint2(c0, c1);
-      q.scales[b] = (uint8_t)sc;
+#pragma unroll
+  for (int t = 0; t < kSlots; ++t) {
+    const uint32_t b = threadIdx.x + t * kThreads;
+    if (b < n_blocks) {
+      uint32_t c0, c1, sc;
+      if (g > kHugeScale)
+        sc = quantize_block<true>(v[t], g, gd6, c0, c1);
+      else
+        sc = quantize_block<false>(v[t], g, gd6, c0, c1);
+      reinterpret_cast<uint2*>(lds_codes)[b] = make_uint2(c0, c1);
+      lds_scales[b] = (uint8_t)sc;
+      if (out) {
+        reinterpret_cast<uint2*>(q.codes)[b] = make_uint2(c0, c1);
+        q.scales[b] = (uint8_t)sc;
+      }
     }
   }
   __syncthreads();
@@ -440,12 +453,16 @@ hipError_t launch_splitk_narrow(const GemmOperands& o, GemmParams p, bool out_f3
 }
 
 // Activations of at most kDecodePrivateRows rows take the private rings (no
-// barrier; their activation loads are a few rows of 32 bytes per chunk), more
-// rows the shared line-group ring.
-constexpr uint32_t kDecodePrivateRows = 8;
+// barrier; their activation loads are a few rows of 32 bytes per chunk) and
+// one weight fragment per workgroup (twice the workgroups, five per CU: 1 and
+// 7 rows against the gate/up weight 30.6 -> 28.7 and 30.9 -> 29.1 us, same
+// box); more rows the shared line-group ring with two weight fragments (one
+// fragment would repeat the activation loads in twice the workgroups).  Each
+// output column's sum runs in the same order either way.
+constexpr uint32_t kDecodePrivateRows = 8;   // the kSplitkDecodeFew plan (gemm.hip) takes the same bound
 
 hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f32, hipStream_t stream) {
-  if (p.M <= kDecodePrivateRows) return launch_splitk<4, 1, 2, 3, false>(o, p, out_f32, false, stream);
+  if (p.M <= kDecodePrivateRows) return launch_splitk<4, 1, 1, 3, false>(o, p, out_f32, false, stream);
   return launch_splitk<4, 1, 2, 3, true>(o, p, out_f32, false, stream);
 }
 

@@ -268,7 +268,7 @@ size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
 // the quantizer launch in front of the GEMM (1 token: 33.0 vs 34.5 us on
 // the gate/up weight read from HBM); at 7 tokens the repeated quantization
 // already costs more than the launch (43.6 vs 36.7 us).
-constexpr int64_t kDecodeFuseMaxElems = 16384;
+constexpr int64_t kDecodeFuseMaxElems = 16 * (int64_t)kDecodeFuseMaxBlocks;
 
 }  // namespace
 

@@ -239,7 +239,7 @@ def test_gemm_full_workloads(name):
     # BF16 output is the RNE of the FP32 output, everywhere.
     assert torch.equal(y16.contiguous().view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
     kernels = L.gemm_kernels(cfg.m, cfg.n, cfg.k)
-    tile = 64 if "64x96" in kernels[0] else (32 if "32x64" in kernels[0] else 256)
+    tile = 64 if "64x96" in kernels[0] else (32 if ("32x64" in kernels[0] or "32x32" in kernels[0]) else 256)
     rows = _sample_rows(cfg.m, tile)
     log("%s: oracle on %d rows (%d-row tiles: one per tile + a full band), kernels %s" % (
         name, len(rows), tile, kernels))
