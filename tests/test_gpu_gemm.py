@@ -103,11 +103,11 @@ def test_gemm_tail_columns(k, use_ws):
     # full rounds (two tile columns) run as a second launch: 256 x 128 tiles
     # (nvfp4_gemm, or K % 512 != 0), or, with a workspace and K = 512, the
     # square tiles as two K halves (FP32 partials, then the summing pass).
-    # Ragged M and N (a tail 356 columns wide, not a multiple of 8) inside
-    # that tail.  K = 512 runs the scale super-stage kernel for the first
-    # launch.  Every element is checked.
+    # Ragged M and N (a tail 357 columns wide: the partial-sum rows are
+    # padded to 360) inside that tail.  K = 512 runs the scale super-stage
+    # kernel for the first launch.  Every element is checked.
     rng = np.random.default_rng(304 + k)
-    m, n = 300, 129 * 256 + 100
+    m, n = 300, 129 * 256 + 101
     x, w = _xw(rng, m, n, k)
     offs = [0, 20000, 33000, n]
     y32, y16, _, _ = run_gpu(x, w, offs, use_ws=use_ws)
@@ -150,6 +150,11 @@ def test_gemm_last_round_as_k_halves_one_tile():
     np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
                                   bf16_rne_of(y32.contiguous()))
     assert torch.equal(y32[:, : n - 256], y_nows[:, : n - 256])
+    # strided output rows: the same values
+    y_str = torch.empty((m, n + 8), dtype=torch.float32, device="cuda")[:, :n]
+    L.gemm(aq, pw, out=y_str)
+    torch.cuda.synchronize()
+    assert torch.equal(y_str, y32)
     # a workspace one byte short is refused
     with pytest.raises(C.Nvfp4Error):
         L.gemm(aq, pw, out=y32, workspace=torch.empty(need - 1, dtype=torch.uint8, device="cuda"))
