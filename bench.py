@@ -43,6 +43,11 @@ GEMM_SOURCES = ["paper_2609_04098_amd/csrc/gemm.hip", "paper_2609_04098_amd/csrc
                 "paper_2609_04098_amd/csrc/gemm_lds.h", "paper_2609_04098_amd/csrc/gemm_lds_super.hip",
                 "paper_2609_04098_amd/csrc/packed_layout.h", "paper_2609_04098_amd/csrc/launch.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_mlp_gate_up_traffic.md")
+# After host-side set-up the GPU's clock ramps back up over roughly 25 ms of
+# back-to-back work (the GEMM's first launches after idle take 2.6-2.8 ms,
+# then 2.3, 2.2 and 2.17 ms from about the tenth launch on), so every warmup
+# continues past its W calls until this much GPU time has run.
+SETTLE_MS = 60.0
 
 
 def log(msg):
@@ -107,6 +112,27 @@ def cpu_baseline(cfg, x_bits, w_bits, rows=8192, cols_per_seg=17408):
     }
 
 
+def warm(fn, warmup, stream, min_ms=SETTLE_MS):
+    """Runs fn untimed `warmup` times, then further until at least `min_ms`
+    of GPU time has passed since the first call (clock settling); returns
+    the number of calls made."""
+    import torch
+    first = torch.cuda.Event(enable_timing=True)
+    last = torch.cuda.Event(enable_timing=True)
+    first.record(stream)
+    n = 0
+    batch = max(1, warmup)
+    while True:
+        for _ in range(batch):
+            fn()
+        n += batch
+        last.record(stream)
+        last.synchronize()
+        if first.elapsed_time(last) >= min_ms or n >= 5000:
+            return n
+        batch = max(1, n)
+
+
 def measure_workload(name, steps, warmup, dev, log_fn):
     """GEMM and dynamic act-quant of one more workload, timed like the
     headline step (HIP events on the launch stream around each launch);
@@ -127,9 +153,11 @@ def measure_workload(name, steps, warmup, dev, log_fn):
     gws = L.gemm_workspace(cfg.m, cfg.n, cfg.k, dev)
     y = torch.empty((cfg.m, cfg.n), dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
-    for _ in range(warmup):
+    def step():
         L.quantize_act(x, out=aq, workspace=ws)
         L.gemm(aq, pw, out=y, workspace=gws)
+
+    warm(step, warmup, stream)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     for i in range(steps):
         ev[i][0].record(stream)
@@ -161,8 +189,7 @@ def measure_workload(name, steps, warmup, dev, log_fn):
         rng = np.random.default_rng(99)
         a_log = torch.from_numpy(np.log(rng.uniform(1.0, 16.0, h)).astype(np.float32)).to(dev)
         dt_bias = torch.from_numpy(rng.uniform(-4.0, 2.0, h).astype(np.float32)).to(dev)
-        for _ in range(warmup):
-            L.gemm_gdn_gates(aq, pw, a_log, dt_bias, out=y)
+        warm(lambda: L.gemm_gdn_gates(aq, pw, a_log, dt_bias, out=y), warmup, stream)
         gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
         for i in range(steps):
             gev[i][0].record(stream)
@@ -180,8 +207,7 @@ def measure_workload(name, steps, warmup, dev, log_fn):
             wsp = ws if mode == C.NVFP4_DYNAMIC else None
             call = lambda: C.nvfp4_quantize_gemm(x, gb, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, mode, wsp,
                                                  stream=stream)
-            for _ in range(warmup):
-                call()
+            warm(call, warmup, stream)
             fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
             for i in range(steps):
                 fev[i][0].record(stream)
@@ -227,8 +253,7 @@ def measure_decode(pw, m, steps, warmup, dev):
 
     res = {"M": m, "N": pw.n, "K": cfg.k, "w_bytes": int(pw.packed.numel())}
     for name, fn in (("unfused", unfused), ("fused", fused)):
-        for _ in range(warmup):
-            fn()
+        warm(fn, warmup, stream)
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
         for i in range(steps):
             flush.sum()
@@ -311,9 +336,8 @@ def main():
         if ev is not None:
             ev[2].record(stream)
 
-    log("warmup %d steps" % args.warmup)
-    for _ in range(args.warmup):
-        step()
+    log("warmup %d steps (continued until %.0f ms of GPU time)" % (args.warmup, SETTLE_MS))
+    warmup_run = warm(step, args.warmup, stream)
     torch.cuda.synchronize()
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
@@ -393,8 +417,7 @@ def main():
             wsp = ws if mode == C.NVFP4_DYNAMIC else None
             call = lambda: C.nvfp4_quantize_gemm(x, gb, pw.packed, pw.n, pw.seg_offsets, pw.g_seg, y, mode, wsp,
                                                  stream=stream)
-            for _ in range(args.warmup):
-                call()
+            warm(call, args.warmup, stream)
             fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
             for i in range(args.steps):
                 fev[i][0].record(stream)
@@ -417,6 +440,9 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warmup_run,
+        "warmup_note": "untimed steps continue past W until %.0f ms of GPU time have run (clock settling "
+                       "after host-side set-up)" % SETTLE_MS,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

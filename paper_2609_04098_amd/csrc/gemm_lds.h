@@ -43,6 +43,11 @@ struct LdsCfg {
   static constexpr int kStages = kStages_;
   static constexpr int kSuperBase = kStages * kStageBytes;
   static constexpr int kLdsBytes = kSuperBase + (kSuper ? 2 * kSuperBytes : 0);
+  // BF16 epilogue staging, beyond the ring (so that no wave waits for the
+  // others to leave the ring): per wave 32 output rows of its FN fragment
+  // columns, rows padded by 16 bytes.
+  static constexpr int kEpiPitch = FN * 32 * 2 + 16;
+  static constexpr int kEpiBytes = kWaves * 32 * kEpiPitch;
   // DMA loads per chunk and wave (without the super-stage loads).
   static constexpr int kLoadsPerWave = kAPerWave + kBPerWave + (kSuper ? 0 : kSDmaA + kSDmaB);
   static constexpr int kSuperLoads = 2;          // per 4 chunks: one A pair, one W pair
@@ -61,7 +66,7 @@ struct LdsCfg {
   static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerWave < 64, "ring depth");
   static_assert(NFA % kWaves == 0 && NFB % kWaves == 0 && kAPerWave > 0 && kBPerWave > 0, "load split");
   static_assert(kLdsReads <= kMfma / 2 && kLoadsPerWave <= kMfma, "schedule slots");
-  static_assert(kOcc * kLdsBytes <= 160 * 1024, "LDS per CU");
+  static_assert(kOcc * (kLdsBytes + kEpiBytes) <= 160 * 1024, "LDS per CU");
 };
 
 // The launched shape: 256 x 256 workgroups of 2 x 2 waves, each wave a
@@ -79,6 +84,109 @@ typedef LdsCfg<2, 2, 4, 4, 1, 5, 4, true> LdsSquareSuper;
 typedef LdsCfg<2, 2, 4, 2, 2, 5, 4> LdsTall;
 static_assert(LdsSquare::BM == kSquareTile && LdsSquare::BN == kSquareTile && LdsSquareSuper::BN == kSquareTile,
               "square tile of the dispatch");
+
+// BF16 epilogue of the LDS kernel: y = RNE_bf16(acc / (G_A G_W[s])) for the
+// segment s of each column.  Accumulator fragment (fa, fb) is transposed:
+// lane (h, r) holds output row m0 + 32 fa + r and, in entries 4 q .. 4 q + 3,
+// the adjacent columns n0 + 32 fb + 8 q + 4 h + (0..3).  A whole wave block
+// (all rows < M, all columns < N, one segment) with rows starting on 16-byte
+// boundaries moves through the wave's own LDS staging area 32 rows at a time:
+// each lane writes 8 bytes (4 columns) of one row, then every global store
+// writes 16 bytes of one row, 4 lanes covering the 32 columns of a fragment
+// and 16 rows per instruction (a dword per column pair spread over 4 rows
+// per instruction took 3 times as long per tile in isolation, and the
+// epilogue 4.8 instead of 3.3 us per tile on mlp_gate_up).  Other blocks
+// (partial, unaligned, or with a segment boundary inside the wave's columns)
+// are stored element by element.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Fast-path test and column scale of the BF16 epilogue, taken before the K
+// loop so that the scale loads stay off the epilogue's path.
+struct EpiPlan {
+  bool whole;     // stage the wave block through LDS with one column scale
+  float alpha;    // that scale
+};
+
+__device__ __forceinline__ int segment_of(const GemmParams& p, uint32_t col) {
+  int s = 0;
+#pragma unroll
+  for (int i = 1; i < NVFP4_SEG_TABLE - 1; ++i) s += (i < p.n_seg && col >= p.seg_off[i]) ? 1 : 0;
+  return s;
+}
+
+__device__ __forceinline__ float segment_scale(const float* __restrict__ a_g, const float* __restrict__ w_g, int s) {
+  const float prod = *a_g * w_g[s];
+  return prod == 0.0f ? 0.0f : 1.0f / prod;
+}
+
+template <int FM, int FN>
+__device__ __forceinline__ EpiPlan epi_plan(const GemmParams& p, const float* __restrict__ a_g,
+                                            const float* __restrict__ w_g, const void* y, uint32_t m0, uint32_t n0) {
+  const uint32_t n_last = (n0 + FN * 32u < p.N ? n0 + FN * 32u : p.N) - 1u;
+  const int s0 = segment_of(p, n0);
+  EpiPlan e;
+  e.whole = m0 + FM * 32u <= p.M && n0 + FN * 32u <= p.N && ((p.ldy * 2u) & 15u) == 0 &&
+            (reinterpret_cast<uintptr_t>(y) & 15u) == 0 && s0 == segment_of(p, n_last);
+  e.alpha = segment_scale(a_g, w_g, s0);
+  return e;
+}
+
+template <int FM, int FN, int kPitch>
+__device__ __forceinline__ void store_tile_t(const floatx16 (&acc)[FM][FN], const GemmParams& p, EpiPlan ep,
+                                             const float* __restrict__ a_g, const float* __restrict__ w_g,
+                                             void* __restrict__ y, uint32_t m0, uint32_t n0, uint32_t lane,
+                                             uint8_t* stage) {
+  constexpr uint32_t E = 2u;                      // bytes per output element
+  const uint32_t r = lane & 31u, h = lane >> 5;
+  if (ep.whole) {
+    const float alpha = ep.alpha;
+    constexpr uint32_t kPieces = 2u * E;          // 16-byte pieces per fragment row
+    constexpr uint32_t kRows = 64u / kPieces;     // rows per store instruction
+    const uint32_t rr = lane / kPieces, pc = lane % kPieces;
+#pragma unroll
+    for (int fa = 0; fa < FM; ++fa) {
+#pragma unroll
+      for (int fb = 0; fb < FN; ++fb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const floatx16& v = acc[fa][fb];
+          const uint32_t lo = pack_bf16_rne(v[4 * q] * alpha, v[4 * q + 1] * alpha);
+          const uint32_t hi = pack_bf16_rne(v[4 * q + 2] * alpha, v[4 * q + 3] * alpha);
+          *reinterpret_cast<u32x2*>(stage + r * kPitch + (fb * 32u + q * 8u + h * 4u) * E) = u32x2{lo, hi};
+        }
+      // Lanes read what other lanes wrote, and the next fragment row
+      // overwrites what they read: keep the LDS accesses in program order.
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+      for (uint32_t k = 0; k < 32u / kRows; ++k)
+#pragma unroll
+        for (int fb = 0; fb < FN; ++fb) {
+          const uint32_t row = k * kRows + rr;
+          const int4v v = *reinterpret_cast<const int4v*>(stage + row * kPitch + fb * 32u * E + pc * 16u);
+          uint8_t* d = static_cast<uint8_t*>(y) + ((size_t)(m0 + fa * 32u + row) * p.ldy + n0 + fb * 32u) * E;
+          *reinterpret_cast<int4v*>(d + pc * 16u) = v;
+        }
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    }
+    return;
+  }
+#pragma unroll
+  for (int fb = 0; fb < FN; ++fb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t col = n0 + fb * 32u + q * 8u + h * 4u + i;
+        if (col >= p.N) continue;
+        const float a = segment_scale(a_g, w_g, segment_of(p, col));
+#pragma unroll
+        for (int fa = 0; fa < FM; ++fa) {
+          const uint32_t row = m0 + fa * 32u + r;
+          if (row < p.M)
+            static_cast<uint16_t*>(y)[(size_t)row * p.ldy + col] = f32_to_bf16_rne(acc[fa][fb][4 * q + i] * a);
+        }
+      }
+}
 
 template <class C, bool kF32Out>
 __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const uint8_t* __restrict__ a_codes,
@@ -207,6 +315,16 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
     }
   };
 
+  // BF16 output: acc[fa][fb] holds the transposed output block of fragments
+  // (fa, fb) (the MFMAs take the weight fragment as their first operand),
+  // for the staged epilogue.  FP32 output keeps the direct orientation and
+  // per-element stores, whose 32 lanes write 128 contiguous bytes of a row
+  // (the staged form measured 3% slower there, and its instantiation's
+  // main loop compiled worse).
+  constexpr bool kTransposed = !kF32Out;
+  const uint32_t m0_wave = tm * BM + wm * FM * 32, n0_wave = p.n_off + tn * BN + wn * FN * 32;
+  EpiPlan ep{};
+  if constexpr (kTransposed) ep = epi_plan<FM, FN>(p, a_g, w_g, y, m0_wave, n0_wave);
   floatx16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -267,7 +385,9 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
       for (int fa = 0; fa < FM; ++fa)
 #pragma unroll
         for (int fb = 0; fb < FN; ++fb)
-          acc[fa][fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
+          acc[fa][fb] = kTransposed
+                            ? __builtin_amdgcn_mfma_f32_32x32x16_f16(bv[u][fb], av[u][fa], acc[fa][fb], 0, 0, 0)
+                            : __builtin_amdgcn_mfma_f32_32x32x16_f16(av[u][fa], bv[u][fb], acc[fa][fb], 0, 0, 0);
     }
     // LDS reads spread over the first half of the chunk, DMA issues over the
     // first three quarters.
@@ -318,7 +438,13 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   // Drain the DMA of the chunks past the end before the workgroup exits.
   __builtin_amdgcn_s_waitcnt(0x0F70);
   void* yo = kF32Out ? static_cast<void*>(static_cast<float*>(y) + (size_t)part * p.part_stride) : y;
-  store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, yo, tm * BM + wm * FM * 32, p.n_off + tn * BN + wn * FN * 32, r, h);
+  if constexpr (kTransposed) {
+    constexpr int kPitch = C::kEpiPitch;
+    store_tile_t<FM, FN, kPitch>(acc, p, ep, a_g, w_g, yo, m0_wave, n0_wave, lane,
+                                 smem + C::kLdsBytes + wave * 32 * kPitch);
+  } else {
+    store_tile<FM, FN, kF32Out>(acc, p, a_g, w_g, yo, m0_wave, n0_wave, r, h);
+  }
 }
 
 // Output columns [n_begin, n_end) (n_begin a multiple of 32).
@@ -329,7 +455,8 @@ static hipError_t launch_lds_as(const GemmOperands& o, GemmParams p, uint32_t n_
   p.tiles_m = (p.M + C::BM - 1) / C::BM;
   p.tiles_n = (n_end - n_begin + C::BN - 1) / C::BN;
   const dim3 grid(p.tiles_m * p.tiles_n * p.k_parts), block(C::kThreads);
-  hipLaunchKernelGGL((gemm_lds_kernel<C, kF32Out>), grid, block, C::kLdsBytes, stream, o.a_codes, o.a_scales, o.a_g,
+  const uint32_t lds = C::kLdsBytes + (kF32Out ? 0 : C::kEpiBytes);
+  hipLaunchKernelGGL((gemm_lds_kernel<C, kF32Out>), grid, block, lds, stream, o.a_codes, o.a_scales, o.a_g,
                      o.w_packed, o.w_g, o.y, p);
   return hipGetLastError();
 }

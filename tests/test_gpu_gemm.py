@@ -184,6 +184,37 @@ def test_gemm_strided_output():
     check_small(x, w, [0, 64, 136], ldy=256, what="ldy")
 
 
+@pytest.mark.parametrize("ldy,col0", [(768, 0), (771, 0), (776, 1), (776, 8)])
+def test_gemm_bf16_rows_staged_or_not(ldy, col0):
+    # The prefill kernel's bf16 epilogue stages whole wave blocks through
+    # LDS and stores 16 bytes of a row per lane when every output row starts
+    # on a 16-byte boundary (ldy = 768, or 776 at an 8-column offset), and
+    # stores element by element otherwise (ldy = 771; or the output shifted
+    # by one column).  Segment boundaries on multiples of 256 keep every
+    # wave block in one segment.  Every bf16 value must be RNE of the FP32
+    # output, and nothing outside the output may be written.
+    rng = np.random.default_rng(307)
+    m, n, k = 512, 768, 256
+    x, w = _xw(rng, m, n, k)
+    offs = [0, 256, n]
+    aq = L.quantize_act(to_dev_bf16(x))
+    pw = L.pack_weight(to_dev_bf16(w), offs)
+    y32 = L.gemm(aq, pw, out_dtype=torch.float32)
+    big = torch.full((m, ldy), -7.0, dtype=torch.bfloat16, device="cuda")
+    y16 = big[:, col0:col0 + n]
+    assert y16.stride(0) == ldy
+    L.gemm(aq, pw, out=y16)
+    torch.cuda.synchronize()
+    xp, xs, gx = OQ.quantize_tensor(x)
+    wp, ws, gw = OQ.quantize_segments(w, offs)
+    check_gemm(y32.cpu().numpy().astype(np.float64), OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs),
+               OG.abs_bound(xp, xs, gx, wp, ws, gw, offs), "ldy %d col0 %d" % (ldy, col0))
+    np.testing.assert_array_equal(y16.contiguous().view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_of(y32))
+    rest = torch.cat([big[:, :col0].flatten(), big[:, col0 + n:].flatten()])
+    assert bool((rest == -7.0).all())
+
+
 def test_gemm_segments_with_very_different_scales():
     rng = np.random.default_rng(301)
     k = 256
