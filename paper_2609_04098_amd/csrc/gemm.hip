@@ -116,6 +116,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   if (M == 0) return hipSuccess;
   GemmParams p = gemm_params(M, K, N, seg_offsets, n_seg, ldy);
   p.y_pairs = (ldy % 2 == 0) && (reinterpret_cast<uintptr_t>(y) % 4 == 0) ? 1u : 0u;
+  p.y_stream = !out_f32 && (uint64_t)M * (uint64_t)N * 2u >= kMallBytes ? 1u : 0u;
   const GemmOperands o{a_codes, a_scales, a_g, static_cast<const uint8_t*>(w_packed), w_g, y};
   GemmPlan g = plan_gemm(M, N, K, cu_count(), workspace != nullptr);
   if (g.second == GemmPlan::kLdsSuperHalves && workspace_bytes < plan_workspace_bytes(g, M, N))

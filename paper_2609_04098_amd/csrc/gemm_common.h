@@ -85,6 +85,11 @@ struct GemmParams {
   int n_seg;
   uint32_t seg_off[NVFP4_SEG_TABLE];
   uint32_t y_pairs;          // bf16 output: y and ldy allow dword stores of column pairs
+  // BF16 output at least as large as the MALL: the LDS kernel's staged
+  // stores are non-temporal (the output cannot stay cached, and its lines
+  // go to HBM while the GEMM leaves HBM idle instead of being written back
+  // when the next kernel's reads evict them).
+  uint32_t y_stream;
   // K split across workgroups (LDS kernel, FP32 output only): k_parts = 2
   // runs every tile twice, workgroup 2t + j on chunks [j * chunks, (j + 1) *
   // chunks) writing its partial sums at y + j * part_stride floats.
@@ -395,6 +400,9 @@ inline GemmParams gemm_params(int64_t M, int64_t K, int64_t N, const int64_t* se
     p.seg_off[i] = (uint32_t)seg_offsets[i <= n_seg ? i : n_seg];
   return p;
 }
+
+// MALL (last-level memory-side cache) of the MI355X.
+constexpr uint64_t kMallBytes = 256ull << 20;
 
 // Side of the square prefill tile (gemm_lds_kernel<LdsSquare*>).
 constexpr uint32_t kSquareTile = 256;

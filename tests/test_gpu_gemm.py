@@ -215,6 +215,36 @@ def test_gemm_bf16_rows_staged_or_not(ldy, col0):
     assert bool((rest == -7.0).all())
 
 
+def test_gemm_bf16_output_larger_than_mall():
+    # A bf16 output of at least 256 MB (8192 x 16640: 272 MB) is written with
+    # non-temporal stores; the same product for the first 512 rows (17 MB,
+    # ordinary stores) must give the same bits, and every bf16 value must
+    # be RNE of the FP32 output.
+    rng = np.random.default_rng(308)
+    m, n, k = 8192, 16640, 256
+    x, w = _xw(rng, m, n, k)
+    offs = [0, 8192, n]
+    aq = L.quantize_act(to_dev_bf16(x))
+    pw = L.pack_weight(to_dev_bf16(w), offs)
+    y16 = L.gemm(aq, pw)
+    y32 = L.gemm(aq, pw, out_dtype=torch.float32)
+    assert torch.equal(y16.view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
+    del y32
+    aq_top = L.quantize_act(to_dev_bf16(x[:512]), g=aq.g.item())    # the whole tensor's global scale
+    y_top = L.gemm(aq_top, pw)
+    torch.cuda.synchronize()
+    assert torch.equal(y16[:512].view(torch.int16), y_top.view(torch.int16))
+    rows = np.arange(0, m, 509)
+    xp, xs, gx = OQ.quantize_tensor(x)
+    wp, ws, gw = OQ.quantize_segments(w, offs)
+    y_ref = OG.gemm_f64(xp, xs, gx, wp, ws, gw, offs, rows=rows)
+    r_ref = OG.abs_bound(xp, xs, gx, wp, ws, gw, offs, rows=rows)
+    got = y16[torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
+    # bf16 output: within the GEMM tolerance plus half a bf16 step
+    err = np.abs(got - y_ref)
+    assert (err <= 1e-4 * r_ref + np.abs(y_ref) * 2.0 ** -8 + 1e-30).all()
+
+
 def test_gemm_segments_with_very_different_scales():
     rng = np.random.default_rng(301)
     k = 256
