@@ -98,11 +98,12 @@ static_assert(LdsSquare::BM == kSquareTile && LdsSquare::BN == kSquareTile && Ld
 // epilogue 4.8 instead of 3.3 us per tile on mlp_gate_up).  Other blocks
 // (partial, unaligned, or with a segment boundary inside the wave's columns)
 // are stored element by element.  The staged stores are non-temporal when
-// the output is at least as large as the MALL (p.y_stream): with ordinary
-// stores, the dirty lines of mlp_gate_up's 570 MB output were written back
-// during the next step's activation amax pass (dynamic act-quant 48.7 ->
-// 35.2 us with non-temporal stores, the GEMM 0.35% longer, the step the same
-// or 0.3% shorter, same box).
+// the output is at least as large as the MALL (p.y_stream), each
+// instruction then writing 4 whole rows of the wave block (256 bytes each):
+// with ordinary stores, the dirty lines of mlp_gate_up's 570 MB output were
+// written back during the next step's activation amax pass (dynamic
+// act-quant 47.3 -> 36.4 us in the step, the GEMM and the step 0.5-0.9%
+// shorter, same box).
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kCachePolicyNonTemporal = 2;   // the "nt" bit of a gfx950 buffer instruction
 
@@ -149,6 +150,8 @@ __device__ __forceinline__ void store_tile_t(const floatx16 (&acc)[FM][FN], cons
     constexpr uint32_t kPieces = 2u * E;          // 16-byte pieces per fragment row
     constexpr uint32_t kRows = 64u / kPieces;     // rows per store instruction
     const uint32_t rr = lane / kPieces, pc = lane % kPieces;
+    constexpr uint32_t kLanesWide = FN * kPieces, kRowsWide = 64u / kLanesWide;   // whole wave-block rows
+    const uint32_t rw = lane / kLanesWide, pw = lane % kLanesWide;
     // Non-temporal stores go through a buffer descriptor: a plain store in
     // the other branch would be merged with a non-temporal one (dropping
     // the hint).
@@ -167,19 +170,29 @@ __device__ __forceinline__ void store_tile_t(const floatx16 (&acc)[FM][FN], cons
       // Lanes read what other lanes wrote, and the next fragment row
       // overwrites what they read: keep the LDS accesses in program order.
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      // Byte offsets in y stay below 2^32 (the API bounds M * ldy by 2^31).
+      if (p.y_stream) {
+        // Non-temporal: whole 128-byte lines per instruction (a row of the
+        // wave block per FN * 4 lanes); 64-byte pieces wrote 1.38 times the
+        // output bytes to HBM this way.
 #pragma unroll
-      for (uint32_t k = 0; k < 32u / kRows; ++k)
-#pragma unroll
-        for (int fb = 0; fb < FN; ++fb) {
-          const uint32_t row = k * kRows + rr;
-          const int4v v = *reinterpret_cast<const int4v*>(stage + row * kPitch + fb * 32u * E + pc * 16u);
-          // Byte offset in y (below 2^32: the API bounds M * ldy by 2^31).
-          const uint32_t off = ((m0 + fa * 32u + row) * p.ldy + n0 + fb * 32u) * E + pc * 16u;
-          if (p.y_stream)
-            __builtin_amdgcn_raw_buffer_store_b128(v, ry, off, 0, kCachePolicyNonTemporal);
-          else
-            *reinterpret_cast<int4v*>(static_cast<uint8_t*>(y) + off) = v;
+        for (uint32_t k = 0; k < 32u / kRowsWide; ++k) {
+          const uint32_t row = k * kRowsWide + rw;
+          const int4v v = *reinterpret_cast<const int4v*>(stage + row * kPitch + pw * 16u);
+          const uint32_t off = ((m0 + fa * 32u + row) * p.ldy + n0) * E + pw * 16u;
+          __builtin_amdgcn_raw_buffer_store_b128(v, ry, off, 0, kCachePolicyNonTemporal);
         }
+      } else {
+#pragma unroll
+        for (uint32_t k = 0; k < 32u / kRows; ++k)
+#pragma unroll
+          for (int fb = 0; fb < FN; ++fb) {
+            const uint32_t row = k * kRows + rr;
+            const int4v v = *reinterpret_cast<const int4v*>(stage + row * kPitch + fb * 32u * E + pc * 16u);
+            const uint32_t off = ((m0 + fa * 32u + row) * p.ldy + n0 + fb * 32u) * E + pc * 16u;
+            *reinterpret_cast<int4v*>(static_cast<uint8_t*>(y) + off) = v;
+          }
+      }
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
     return;
