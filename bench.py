@@ -22,6 +22,7 @@ Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
 """
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -222,13 +223,16 @@ def measure_workload(name, steps, warmup, dev, log_fn):
     return out
 
 
-def measure_decode(pw, m, steps, warmup, dev):
+def measure_decode(pws, m, steps, warmup, dev):
     """Decode-shaped calls against the headline's gate/up weight (34816 x
     5120, two segments): m rows of residual-stream X (the 32-token decode
     workload's first rows), dynamic G.  Unfused (quantizer + GEMM, two or
     three launches) and fused (nvfp4_quantize_gemm, one launch).  Before
-    every timed call a 640 MB read evicts the weight from the 256 MB MALL,
-    as successive layers of a model would; HIP events, median."""
+    every timed call a 640 MB read evicts the weight from the 256 MB MALL;
+    HIP events, median.  Sustained: back-to-back calls on 8 copies of the
+    packed weight in turn (800 MB, as successive layers of a model would
+    read their own weights from HBM), time per call."""
+    pw = pws[0]
     import numpy as np
     import torch
     from paper_2609_04098_amd import linear as L
@@ -244,12 +248,12 @@ def measure_decode(pw, m, steps, warmup, dev):
     y = torch.empty((m, pw.n), dtype=torch.bfloat16, device=dev)
     flush = torch.ones(160 << 20, dtype=torch.float32, device=dev)
 
-    def unfused():
+    def unfused(w=pw):
         L.quantize_act(x, out=aq, workspace=ws)
-        L.gemm(aq, pw, out=y)
+        L.gemm(aq, w, out=y)
 
-    def fused():
-        L.quantize_gemm(x, pw, out=y, workspace=wsq)
+    def fused(w=pw):
+        L.quantize_gemm(x, w, out=y, workspace=wsq)
 
     res = {"M": m, "N": pw.n, "K": cfg.k, "w_bytes": int(pw.packed.numel())}
     for name, fn in (("unfused", unfused), ("fused", fused)):
@@ -265,6 +269,16 @@ def measure_decode(pw, m, steps, warmup, dev):
         res[name + "_median_ms"] = round(ms, 4)
         res[name + "_w_gbs"] = round(pw.packed.numel() / (ms * 1e-3) / 1e9, 1)
         res[name + "_frac_hbm"] = round(pw.packed.numel() / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        calls = 8 * max(2, steps // 4)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(calls):
+            fn(pws[i % len(pws)])
+        b.record(stream)
+        torch.cuda.synchronize()
+        sus = a.elapsed_time(b) / calls
+        res[name + "_sustained_ms"] = round(sus, 4)
+        res[name + "_sustained_frac_hbm"] = round(pw.packed.numel() / (sus * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
     del flush
     return res
 
@@ -387,6 +401,29 @@ def main():
         lambda: C.nvfp4_rmsnorm_quantize_act(x, gamma, 1e-6, aq.codes, aq.scales, aq.g, None, stream))
     del flush
 
+    # The same quantizers called back to back (as the layers of a prefill
+    # would) on 8 distinct activations of X's shape (672 MB, more than twice
+    # the MALL, visited in turn so that each is read from HBM): HIP events
+    # around all the calls, time per call.
+    xr = [x] + [torch.roll(x, shifts=17 * i, dims=1) for i in range(1, 8)]
+
+    def time_sustained(fn, calls=32):
+        for i in range(8):
+            fn(xr[i])
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(calls):
+            fn(xr[i % 8])
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / calls
+
+    aq_static_sus = time_sustained(
+        lambda xi: C.nvfp4_quantize_act(xi, aq.codes, aq.scales, aq.g, C.NVFP4_STATIC, None, stream))
+    norm_sus = time_sustained(
+        lambda xi: C.nvfp4_rmsnorm_quantize_act(xi, gamma, 1e-6, aq.codes, aq.scales, aq.g, None, stream))
+    del xr
+
     gates = None
     if cfg.n <= 96 and cfg.n % 2 == 0 and cfg.k % 64 == 0 and len(cfg.segments) == 2:
         # The tall-skinny b|a gate projection with the GDN gate transform
@@ -477,12 +514,18 @@ def main():
         "act_quant_static": {
             "bound": "hbm", "median_ms": round(aq_static_avg, 4), "achieved": round(aq_static_gbs, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(aq_static_gbs / HBM_PEAK_GBS, 4),
-            "note": "one pass with a given (calibrated) global scale, X from HBM (median); not part of value",
+            "sustained_ms": round(aq_static_sus, 4),
+            "sustained_frac": round(aq_bytes / (aq_static_sus * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "note": "one pass with a given (calibrated) global scale, X from HBM: one call after a 640 MB read "
+                    "(median); sustained: back-to-back calls on 8 distinct activations (672 MB); not part of value",
         },
         "rmsnorm_act_quant_static": {
             "bound": "hbm", "median_ms": round(norm_avg, 4), "achieved": round(norm_gbs, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(norm_gbs / HBM_PEAK_GBS, 4),
-            "note": "RMSNorm fused with the static-scale quantizer, one pass, X from HBM (median); not part of value",
+            "sustained_ms": round(norm_sus, 4),
+            "sustained_frac": round(aq_bytes / (norm_sus * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "note": "RMSNorm fused with the static-scale quantizer, one pass, X from HBM (as act_quant_static); "
+                    "not part of value",
         },
         "gdn_gates": gates,
         "fused_quantize_gemm": fused,
@@ -492,7 +535,9 @@ def main():
     }
     if not args.no_other_workloads and args.workload == WORKLOAD:
         log("decode shapes against the gate/up weight")
-        result["decode"] = {"m%d" % m: measure_decode(pw, m, args.steps, args.warmup, dev) for m in (1, 7, 32)}
+        pws = [pw] + [dataclasses.replace(pw, packed=pw.packed.clone()) for _ in range(7)]
+        result["decode"] = {"m%d" % m: measure_decode(pws, m, args.steps, args.warmup, dev) for m in (1, 7, 32)}
+        del pws
         result["other_workloads"] = {}
         for name in ("gdn_qkv", "mlp_down", "ab_gates"):
             result["other_workloads"][name] = measure_workload(name, max(5, args.steps // 2), max(2, args.warmup), dev,
