@@ -448,7 +448,8 @@ hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f3
 constexpr uint32_t kDecodeFuseMaxBlocks = 1024;
 // Activation quantization fused in front of the M <= 32 split-K GEMM, one
 // launch, with the whole quantized activation held in LDS (see
-// gemm_splitk.hip); decode_quant_lds_bytes(M, K) is the LDS it takes.
+// gemm_splitk.hip); decode_quant_lds_bytes(M, K) is the dynamic LDS it takes
+// (the rings; the activation sits in a static 9 KB array).
 struct DecodeQuantArgs {
   const uint16_t* x;        // bf16 [M x K], row stride ldx elements
   uint32_t ldx;

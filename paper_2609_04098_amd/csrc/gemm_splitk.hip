@@ -38,6 +38,16 @@ namespace nvfp4 {
 // bit for bit (same codes, same summation order).  Workgroup 0 also writes
 // G and, when asked for, the codes and scales.
 
+// Workgroup barrier for LDS data only: waits for this wave's LDS accesses,
+// not for its outstanding global loads (__syncthreads' fence would also wait
+// for the weight ring's DMA issued before the activation is quantized).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(lds::kWaitLgkm0);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Maximum over the workgroup (kThreads threads) of a non-negative value.
 template <int kThreads>
 __device__ __forceinline__ uint32_t wg_max_u32(uint32_t v, uint32_t* red) {
@@ -47,11 +57,11 @@ __device__ __forceinline__ uint32_t wg_max_u32(uint32_t v, uint32_t* red) {
     v = v > o ? v : o;
   }
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
+  lds_barrier();
   uint32_t r = red[0];
 #pragma unroll
   for (int w = 1; w < kThreads / 64; ++w) r = r > red[w] ? r : red[w];
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 
@@ -66,25 +76,40 @@ __device__ __forceinline__ void load_x_block(const DecodeQuantArgs& q, uint32_t 
 
 // Quantize all of X into the LDS activation (codes [M][K/2], then scales
 // [M][K/16]); returns G.  X has at most kDecodeFuseMaxBlocks blocks (the
-// launcher's bound): each thread loads its blocks once and keeps them in
-// registers from the maximum to the quantization.
-template <int kThreads, bool kDynamic>
-__device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p, uint8_t* lds_codes,
-                                   uint8_t* lds_scales, uint32_t* red) {
-  constexpr int kSlots = kDecodeFuseMaxBlocks / kThreads;
+// launcher's bound): each thread loads its blocks once (load_x_slots, issued
+// before the weight's first ring stages, so that waiting for X does not
+// wait for them too: the memory counter counts loads in issue order) and
+// keeps them in registers from the maximum to the quantization.
+template <int kThreads>
+struct XSlots {
+  static constexpr int kSlots = kDecodeFuseMaxBlocks / kThreads;
   static_assert(kSlots * kThreads == kDecodeFuseMaxBlocks, "blocks per thread");
-  const uint32_t bpr = p.K >> 4, n_blocks = p.M * bpr;
   uint32_t v[kSlots][8];
+};
+
+template <int kThreads>
+__device__ __forceinline__ void load_x_slots(const DecodeQuantArgs& q, const GemmParams& p, XSlots<kThreads>& xs) {
+  const uint32_t bpr = p.K >> 4, n_blocks = p.M * bpr;
+#pragma unroll
+  for (int t = 0; t < XSlots<kThreads>::kSlots; ++t) {
+    const uint32_t b = threadIdx.x + t * kThreads;
+    if (b < n_blocks) load_x_block(q, b, bpr, xs.v[t]);
+  }
+}
+
+template <int kThreads, bool kDynamic>
+__device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p, XSlots<kThreads>& xs,
+                                   uint8_t* lds_codes, uint8_t* lds_scales, uint32_t* red) {
+  constexpr int kSlots = XSlots<kThreads>::kSlots;
+  const uint32_t bpr = p.K >> 4, n_blocks = p.M * bpr;
+  uint32_t (&v)[kSlots][8] = xs.v;
   uint32_t m = 0;
 #pragma unroll
   for (int t = 0; t < kSlots; ++t) {
     const uint32_t b = threadIdx.x + t * kThreads;
-    if (b < n_blocks) {
-      load_x_block(q, b, bpr, v[t]);
-      if (kDynamic) {
-        const uint32_t a = __float_as_uint(block_amax(v[t]));
-        m = m > a ? m : a;                   // non-negative floats order as integers
-      }
+    if (kDynamic && b < n_blocks) {
+      const uint32_t a = __float_as_uint(block_amax(v[t]));
+      m = m > a ? m : a;                     // non-negative floats order as integers
     }
   }
   float g;
@@ -96,24 +121,33 @@ __device__ float quantize_into_lds(const DecodeQuantArgs& q, const GemmParams& p
   }
   const float gd6 = g * (1.0f / 6.0f);
   const bool out = q.codes != nullptr && blockIdx.x == 0;
+  // All blocks first, then the LDS writes: a write to LDS waits for the
+  // weight ring's direct-to-LDS loads issued before it (the compiler cannot
+  // tell the addresses apart), so the quantization runs before that wait.
+  uint32_t c[kSlots][3];
 #pragma unroll
   for (int t = 0; t < kSlots; ++t) {
     const uint32_t b = threadIdx.x + t * kThreads;
     if (b < n_blocks) {
-      uint32_t c0, c1, sc;
       if (g > kHugeScale)
-        sc = quantize_block<true>(v[t], g, gd6, c0, c1);
+        c[t][2] = quantize_block<true>(v[t], g, gd6, c[t][0], c[t][1]);
       else
-        sc = quantize_block<false>(v[t], g, gd6, c0, c1);
-      reinterpret_cast<uint2*>(lds_codes)[b] = make_uint2(c0, c1);
-      lds_scales[b] = (uint8_t)sc;
+        c[t][2] = quantize_block<false>(v[t], g, gd6, c[t][0], c[t][1]);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < kSlots; ++t) {
+    const uint32_t b = threadIdx.x + t * kThreads;
+    if (b < n_blocks) {
+      reinterpret_cast<uint2*>(lds_codes)[b] = make_uint2(c[t][0], c[t][1]);
+      lds_scales[b] = (uint8_t)c[t][2];
       if (out) {
-        reinterpret_cast<uint2*>(q.codes)[b] = make_uint2(c0, c1);
-        q.scales[b] = (uint8_t)sc;
+        reinterpret_cast<uint2*>(q.codes)[b] = make_uint2(c[t][0], c[t][1]);
+        q.scales[b] = (uint8_t)c[t][2];
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   return g;
 }
 
@@ -275,8 +309,11 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
     uint32_t s[kFrags];
   };
   // LDS-resident activation (fused quantizer): codes [M][K/2], then scales
-  // [M][K/16], after the rings; rows >= M are zero operands.
-  const uint8_t* a_lds = smem + KS * kStages * kStageBytes;
+  // [M][K/16], in a static array apart from the rings (so that its writes
+  // need not wait for the ring's direct-to-LDS loads); rows >= M are zero
+  // operands.
+  __shared__ __attribute__((aligned(16))) uint8_t a_static[kALds ? 9 * kDecodeFuseMaxBlocks : 16];
+  const uint8_t* a_lds = a_static;
   const uint8_t* as_lds = a_lds + p.M * (p.K >> 1);
   auto read_stage = [&](Regs& R, uint32_t i) {
     const uint8_t* st = ring + (i % kStages) * kStageBytes;
@@ -359,12 +396,17 @@ __global__ __launch_bounds__(KS * 64, 2) void gemm_splitk_kernel(const uint8_t* 
     // after it stay in flight (loads land in order).  With the fused
     // quantizer the weight's first stages do not depend on the activation:
     // their loads fly while the workgroup quantizes X into LDS.
+    XSlots<KS * 64> xs;
+    if constexpr (kALds) {
+      load_x_slots<KS * 64>(q, p, xs);
+      __builtin_amdgcn_sched_barrier(0);                 // X's loads first
+    }
 #pragma unroll
     for (int s = 0; s < kStages; ++s) issue_w(s);
     if constexpr (kALds) {
       __shared__ uint32_t red[KS];
-      uint8_t* a_dst = smem + KS * kStages * kStageBytes;
-      const float ga = quantize_into_lds<KS * 64, kQuant == 2>(q, p, a_dst, a_dst + p.M * (p.K >> 1), red);
+      uint8_t* a_dst = a_static;
+      const float ga = quantize_into_lds<KS * 64, kQuant == 2>(q, p, xs, a_dst, a_dst + p.M * (p.K >> 1), red);
       segment_alpha<FN>(p, ga, w_g, n0, r, alpha);
     } else {
       segment_alpha<FN>(p, *a_g, w_g, n0, r, alpha);
@@ -469,11 +511,14 @@ hipError_t launch_splitk_decode(const GemmOperands& o, GemmParams p, bool out_f3
 // The fused decode path's weight ring is one stage deeper than the plain
 // decode kernel's (4 instead of 3: more of the weight in flight while the
 // workgroup quantizes X; one token 33.0 -> 32.6 us, same box), which still
-// leaves three workgroups per CU (36 KB of ring + at most 9 KB of X each).
+// leaves three workgroups per CU (36 KB of ring + the 9 KB static array of
+// the quantized activation each).
 constexpr int kDecodeQuantStages = 4;
 
 size_t decode_quant_lds_bytes(int64_t M, int64_t K) {
-  return (size_t)splitk_ring_bytes<4, 1, 2, kDecodeQuantStages, false>() + (size_t)(M * K / 2 + M * K / 16);
+  (void)M;
+  (void)K;
+  return (size_t)splitk_ring_bytes<4, 1, 2, kDecodeQuantStages, false>();
 }
 
 hipError_t launch_decode_quant_gemm(const GemmOperands& o, GemmParams p, const DecodeQuantArgs& q, bool dynamic,

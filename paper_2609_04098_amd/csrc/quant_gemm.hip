@@ -265,7 +265,7 @@ size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
 // The fused decode kernel quantizes all of X in every workgroup (there is
 // no hand-off between workgroups), so it pays off only while X is a few
 // tokens: up to M * K = 16384 elements (3 tokens of width 5120) it beats
-// the quantizer launch in front of the GEMM (1 token: 33.0 vs 34.5 us on
+// the quantizer launch in front of the GEMM (1 token: 30.2 vs 32.4 us on
 // the gate/up weight read from HBM); at 7 tokens the repeated quantization
 // already costs more than the launch (43.6 vs 36.7 us).
 constexpr int64_t kDecodeFuseMaxElems = 16 * (int64_t)kDecodeFuseMaxBlocks;
