@@ -232,7 +232,9 @@ int nvfp4_harmonize_weight(void* packed, int64_t N, int64_t K,
  *   Y[m, n] = (1 / (G_A * G_W[s])) * sum_k (e S)_A[m, k] (e S)_W[n, k]
  *   for the segment s holding column n.
  * Requirements: M >= 0, N >= 1, K >= 16, K % 16 == 0, M*K, N*K, M*ldy < 2^31.
- * M == 0 enqueues nothing.
+ * M == 0 enqueues nothing.  A bf16 Y of at least 256 MB (the MI355X's
+ * last-level cache) is written with non-temporal stores, so it is not left
+ * in that cache.
  */
 int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                const float* a_g_enc, int64_t M, int64_t K,
