@@ -215,18 +215,24 @@ def test_gemm_bf16_rows_staged_or_not(ldy, col0):
     assert bool((rest == -7.0).all())
 
 
-def test_gemm_bf16_output_larger_than_mall():
+@pytest.mark.parametrize("pad", [0, 8])
+def test_gemm_bf16_output_larger_than_mall(pad):
     # A bf16 output of at least 256 MB (8192 x 16640: 272 MB) is written with
-    # non-temporal stores; the same product for the first 512 rows (17 MB,
-    # ordinary stores) must give the same bits, and every bf16 value must
-    # be RNE of the FP32 output.
+    # non-temporal stores (pad: rows ldy = N + pad apart, still 16-byte
+    # aligned); the same product for the first 512 rows (17 MB, ordinary
+    # stores) must give the same bits, every bf16 value must be RNE of the
+    # FP32 output, and the padding columns must stay untouched.
     rng = np.random.default_rng(308)
     m, n, k = 8192, 16640, 256
     x, w = _xw(rng, m, n, k)
     offs = [0, 8192, n]
     aq = L.quantize_act(to_dev_bf16(x))
     pw = L.pack_weight(to_dev_bf16(w), offs)
-    y16 = L.gemm(aq, pw)
+    big = torch.full((m, n + pad), -7.0, dtype=torch.bfloat16, device="cuda")
+    y16 = big[:, :n]
+    L.gemm(aq, pw, out=y16)
+    if pad:
+        assert bool((big[:, n:] == -7.0).all())
     y32 = L.gemm(aq, pw, out_dtype=torch.float32)
     assert torch.equal(y16.view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
     del y32
