@@ -255,6 +255,7 @@ namespace lds {
 // expcnt [6:4], lgkmcnt [11:8]; all-ones means "do not wait").
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 constexpr int kWaitLgkm0 = 0xC07F;                                    // lgkmcnt(0)
+constexpr int kLgkm0Mask = ~(15 << 8);        // AND into a vmcnt_imm wait: also lgkmcnt(0)
 }  // namespace lds
 
 // 1 / (G_A G_W[s]) for the column of lane r in each of the FN fragment

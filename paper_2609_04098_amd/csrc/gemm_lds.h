@@ -389,16 +389,24 @@ __global__ __launch_bounds__(C::kThreads, C::kOcc) void gemm_lds_kernel(const ui
   auto step = [&](uint32_t c, const Regs& cur, Regs& next, auto pos_tag) {
     constexpr int kPos = decltype(pos_tag)::value;
     constexpr bool kIssueSuper = C::kSuper && kPos == 0;
-    // Every LDS read of the previous iteration has been consumed by its
-    // decode, so after the barrier the stage of chunk c may be refilled.
+    // Wait for chunk c + 1's DMA and for this wave's LDS reads (those of
+    // stage c were issued in the previous iteration), so that after the
+    // barrier the stage of chunk c may be refilled.  The MFMAs and decode of
+    // the previous chunk may still sink past the barrier; they read only
+    // registers.
     if constexpr (C::kSuper)
-      __builtin_amdgcn_s_waitcnt(kPos == 1 || kPos == 2 ? C::kWaitSuper1 : C::kWaitSuper0);
+      __builtin_amdgcn_s_waitcnt((kPos == 1 || kPos == 2 ? C::kWaitSuper1 : C::kWaitSuper0) & lds::kLgkm0Mask);
     else
-      __builtin_amdgcn_s_waitcnt(C::kWaitNext);
+      __builtin_amdgcn_s_waitcnt(C::kWaitNext & lds::kLgkm0Mask);
     __builtin_amdgcn_s_barrier();
     issue(c + kStages);
     if constexpr (kIssueSuper) issue_super((c >> 2) + 1);
     read_stage(next, c + 1);
+    // Square tiles: all LDS reads of chunk c + 1 go out before this chunk's
+    // MFMAs.  Left to the scheduler, half of them sank to just ahead of
+    // their decode at the end of the chunk, each then waited on within one
+    // MFMA (mlp_gate_up 2.17 -> 2.13 ms with the fence).
+    if constexpr (C::kMfma >= 64) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int u = j & 1;
