@@ -131,6 +131,10 @@ def test_quantize_gemm_full_ab_gates():
     (17, 4100, 256, [0, 4000, 4100]),      # many workgroups, few blocks each
     (5, 129, 64, [0, 129]),                # one chunk, N just past the narrow limit
     (20, 300, 2560, [0, 150, 300]),        # 28.8 KB quantized: the two-launch decode path
+    (3, 640, 5120, [0, 320, 640]),         # M * K = 15360: the largest one-launch case at the hidden width
+    (4, 640, 5120, [0, 320, 640]),         # M * K = 20480: the smallest two-launch case there
+    (8, 700, 2048, [0, 350, 700]),         # the most rows with per-wave activation rings
+    (9, 700, 2048, [0, 350, 700]),         # the fewest rows with the shared activation ring
 ])
 def test_quantize_gemm_decode_matches_unfused(m, n, k, offs):
     rng = np.random.default_rng(m * 11 + n * 7 + k)
