@@ -104,6 +104,20 @@ def test_act_quant_small_and_two_pass_paths_agree_on_edge_cases():
     assert_act_matches(z)
 
 
+@pytest.mark.parametrize("m,k", [(256, 256), (4097, 16), (1, 65536), (1, 65552), (64, 1040)])
+def test_act_quant_one_launch_boundary(m, k):
+    # 4096 blocks (256 x 256, one row of 65536) is the largest activation
+    # the one-launch quantizer takes; 4097 blocks go to the two passes;
+    # 64 x 1040 (4160 blocks) is a two-pass shape whose K is not a multiple
+    # of 32.
+    rng = np.random.default_rng(m + k)
+    x = rng.standard_normal((m, k))
+    x[:, rng.choice(k, max(1, k // 200), replace=False)] *= 100.0
+    xb = bits_of(x)
+    assert_act_matches(xb)
+    assert_act_matches(xb, g=np.float32(2688.0 / 50.0))
+
+
 def test_act_quant_special_tensors():
     assert_act_matches(np.zeros((8, 32), dtype=np.uint16))            # G = 0
     z = np.zeros((4, 16), dtype=np.uint16)
