@@ -89,6 +89,8 @@ def test_gemm_tiny_workload():
     (8, 200, 320, [0, 100, 200]),          # small-M, private activation rings (the largest such M)
     (5, 200, 1024, [0, 100, 200]),         # small-M split-K: 4 chunks per wave (one refill)
     (9, 64, 960, [0, 64]),                 # split-K: 15 chunks, 4/4/4/3 per wave
+    (33, 520, 1024, [0, 260, 520]),        # one row past the small-M split-K limit: 256 x 256 tiles, 33 rows
+    (300, 97, 512, [0, 48, 97]),           # one column past the tall-skinny limit: one partial tile column
 ])
 def test_gemm_ragged_shapes(m, n, k, offs):
     rng = np.random.default_rng(m * 7 + n * 3 + k)
